@@ -1,0 +1,318 @@
+/*
+ * atp.h — C ABI of the MI355X state-preserving tensor-parallel reshard
+ * (AnchorTP, arXiv 2511.11617: Sec. III-B elastic TP, Alg. 1 Continuous
+ * Minimal Migration, Eq. 1 minimum reload, Sec. III-C execution scheduler).
+ *
+ * One surviving GPU's share of a TP change k -> k' with unequal widths:
+ *   atp_plan             plan the change on the host (partitions, CMM tasks,
+ *                        new arena layout, copy descriptors, in-place order)
+ *   atp_reshard_weights  repack this GPU's retained weight slices into the
+ *                        new shard layout and land the missing bytes
+ *   atp_reshard_kv       the same for the paged KV cache (block ids kept)
+ *   atp_sync             wait for both, report the first asynchronous error
+ *
+ * Conventions
+ *   - Status: every int-returning call returns ATP_OK (0) or a negative
+ *     ATP_E* code; atp_last_error() returns the message of the last failure
+ *     on the calling thread.
+ *   - Ownership: the caller owns every buffer (arenas, block table, pinned
+ *     host buffers, staging).  The library allocates no device memory; it
+ *     keeps its descriptors, prefix sums and landing ring inside the
+ *     caller's staging buffer.  A plan is a library-owned host object,
+ *     freed with atp_plan_free.
+ *   - Streams: atp_stream is a hipStream_t.  Calls only enqueue work and
+ *     return; atp_sync blocks.
+ *   - Bytes are copied, never converted: any 16-bit payload (NaN, -0,
+ *     denormals) arrives unchanged.
+ *   - Threading: a plan is used by one host thread at a time.
+ */
+#ifndef ATP_H
+#define ATP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+enum {
+  ATP_OK = 0,
+  ATP_EINVAL = -1,    /* malformed problem, bad argument, bad block table  */
+  ATP_ECAPACITY = -2, /* an arena, staging or host buffer is too small     */
+  ATP_EHIP = -3,      /* a HIP runtime call failed                         */
+  ATP_EALIGN = -4,    /* a device buffer is not 256-byte aligned           */
+  ATP_ESTATE = -5     /* call out of order (reshard again before atp_sync) */
+};
+
+typedef void *atp_stream; /* hipStream_t */
+
+/* Half-open range [begin, end) in units of a partition space. */
+typedef struct {
+  int64_t begin, end;
+} atp_range;
+
+/* ---- partition spaces (Sec. III-B, Alg. 1) ------------------------------ */
+/* How the new ranges of a space are obtained.
+ *   EXPLICIT    new_ranges given by the caller (M ranges, in target order)
+ *   FLOOR       Alg. 1: target j = [floor(j H / M), floor((j+1) H / M))
+ *   CEIL_FIRST  Sec. III-B widths ceil(H/M) first, then floor(H/M)
+ *   GQA         ranges follow another (query-head) space's new ranges:
+ *               query heads [a, b) need KV heads [floor(a/g), ceil(b/g))
+ *               with g = gqa_group; ranges may overlap (replicas). */
+enum { ATP_RULE_EXPLICIT = 0, ATP_RULE_FLOOR = 1, ATP_RULE_CEIL_FIRST = 2, ATP_RULE_GQA = 3 };
+
+/* One space: attention heads, KV heads, FFN column groups, experts.
+ * total_units is H; with Alg. 1 it is the largest end of any old range,
+ * dead ranks included.  old_ranges[i] is old rank i's range (N = old_tp of
+ * them, dead ranks included); they may overlap (replicated units) and must
+ * together cover [0, H). */
+typedef struct {
+  int64_t total_units;
+  int32_t old_tp;
+  int32_t new_tp;
+  const atp_range *old_ranges;
+  int32_t new_rule;
+  int32_t gqa_space; /* GQA: index of the query-head space     */
+  int32_t gqa_group; /* GQA: query heads per KV head           */
+  int32_t reserved;
+  const atp_range *new_ranges; /* EXPLICIT: new_tp ranges         */
+} atp_space;
+
+/* ---- tensors (Sec. III-B layout invariants) ----------------------------- */
+/* A weight is the full logical [rows, cols] row-major matrix; the space
+ * shards its rows (ATP_ROWS: column-parallel Wq/Wk/Wv/W_gate/W_up/experts)
+ * or its columns (ATP_COLS: row-parallel Wo/W_down); `unit` rows or
+ * columns make one unit of the space.  old_offset is the byte offset of
+ * this GPU's old shard in the old arena, or ATP_OFFSET_AUTO for the packed
+ * layout (shards in tensor order, each at the next 256-byte boundary).
+ * The new arena always uses the packed layout. */
+enum { ATP_ROWS = 0, ATP_COLS = 1 };
+#define ATP_OFFSET_AUTO UINT64_MAX
+
+typedef struct {
+  int32_t space;
+  int32_t kind;
+  int32_t layer;
+  int32_t elem_bytes;
+  int64_t rows, cols, unit;
+  uint64_t old_offset;
+} atp_tensor;
+
+/* ---- paged KV cache (Sec. III-B: localized by head group per block) ----- */
+/* Arena of one rank: [layer][K,V][num_blocks][heads][block_tokens][head_dim]
+ * (HEAD_MAJOR) or [layer][K,V][num_blocks][block_tokens][heads][head_dim]
+ * (TOKEN_MAJOR), heads = the rank's KV-head range of `space`.  Physical
+ * block ids are unchanged by the reshard; live_blocks is the number of
+ * distinct ids the block table references. */
+enum { ATP_KV_HEAD_MAJOR = 0, ATP_KV_TOKEN_MAJOR = 1 };
+
+typedef struct {
+  int32_t space;
+  int32_t num_layers;
+  int32_t block_tokens;
+  int32_t head_dim;
+  int32_t elem_bytes;
+  int32_t layout;
+  int64_t num_blocks;
+  int64_t live_blocks;
+} atp_kv;
+
+/* ---- problem ------------------------------------------------------------ */
+enum {
+  ATP_ASSIGN_INORDER = 0,   /* target j hosted by the j-th survivor      */
+  ATP_ASSIGN_MAXRETAIN = 1, /* survivor permutation keeping most bytes   */
+  ATP_INPLACE = 1 << 4,     /* new layout overwrites the old arena       */
+  ATP_PLAN_GREEDY = 1 << 8, /* Sec. V baseline: keep local, reload gaps  */
+  ATP_PLAN_FULL = 1 << 9    /* Sec. V baseline: reload every byte        */
+};
+
+typedef struct {
+  int32_t n_spaces;
+  const atp_space *spaces;
+  int32_t n_tensors;
+  const atp_tensor *tensors;
+  const atp_kv *kv;      /* NULL: no KV cache                          */
+  const int32_t *failed; /* old ranks that died                        */
+  int32_t n_failed;
+  int32_t self_old_rank; /* this GPU's old rank (must survive)         */
+  int32_t flags;
+  int32_t reserved;
+  uint64_t staging_cap;  /* in place: staging bytes the schedule may use */
+} atp_problem;
+
+typedef struct atp_plan_obj atp_plan_t;
+
+/* Plan the reshard (Alg. 1 per space, Eq. 1 statistics, Sec. III-C
+ * single-pass pre-allocation: new layout sizes and staging needs, and for
+ * ATP_INPLACE a hazard-free level order with a bounded staging buffer).
+ * Errors: ATP_EINVAL (malformed problem), ATP_ECAPACITY (in-place schedule
+ * needs more than staging_cap).  *out is set only on success. */
+int atp_plan(const atp_problem *problem, atp_plan_t **out);
+void atp_plan_free(atp_plan_t *plan);
+
+/* Repack this GPU's weights (Sec. III-B parameter re-assignment/reload
+ * primitive; Sec. III-C pipelined execution).
+ *   arena        old shard (device, 256-B aligned), arena_bytes long; with
+ *                ATP_INPLACE it must also hold the new layout
+ *   new_arena    destination (device) of new_arena_bytes; NULL with ATP_INPLACE
+ *   inflow_host  pinned host buffer of exactly stats.inflow_w bytes holding
+ *                the bytes this GPU does not keep, in the plan's packing
+ *                order (atp_plan_segments, ATP_SEG_INFLOW_W); stands in for
+ *                peer P2P and host reload
+ *   outbound_host pinned host buffer of stats.outbound_w bytes that receives
+ *                (in place only) the old bytes peers need and this GPU drops,
+ *                read before they are overwritten; may be NULL if 0 bytes
+ *   staging      device scratch of at least stats.staging_w bytes
+ * Launch errors return ATP_EHIP; kernel-side errors surface in atp_sync. */
+int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes,
+                        void *new_arena, uint64_t new_arena_bytes,
+                        const void *inflow_host, uint64_t inflow_bytes,
+                        void *outbound_host, uint64_t outbound_bytes,
+                        void *staging, uint64_t staging_bytes,
+                        atp_stream compute, atp_stream copy);
+
+/* Repack this GPU's paged KV cache (Sec. III-B KV operators with
+ * variable-length shards).  block_table is a device int32
+ * [n_seq][max_blocks], -1 = unused, read only; ids must be < num_blocks
+ * and the distinct ids must number kv.live_blocks (else ATP_EINVAL from
+ * atp_sync).  Buffers as for atp_reshard_weights, sizes from stats.*_kv.
+ * The weights and KV calls may be pending together if their staging
+ * buffers do not overlap. */
+int atp_reshard_kv(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes,
+                   void *new_kv_arena, uint64_t new_kv_bytes,
+                   const int32_t *block_table, int32_t n_seq, int32_t max_blocks,
+                   const void *inflow_host, uint64_t inflow_bytes,
+                   void *outbound_host, uint64_t outbound_bytes,
+                   void *staging, uint64_t staging_bytes,
+                   atp_stream compute, atp_stream copy);
+
+/* Timing of the last reshard (HIP events; host clock for wall_ms). */
+typedef struct {
+  double plan_ms;      /* atp_plan host time                          */
+  double wall_ms;      /* first reshard call -> atp_sync return        */
+  double repack_w_ms;  /* compute-stream span of the weight repack     */
+  double repack_kv_ms; /* compute-stream span of the KV repack         */
+  double h2d_ms;       /* copy-stream span of the inflow copies        */
+  double d2h_ms;       /* span of the outbound copies (in place)       */
+  double scatter_ms;   /* summed landing-ring scatter kernel time      */
+  double overlap;      /* (repack + h2d - wall) / min(repack, h2d)     */
+  uint64_t repack_bytes;  /* algorithmic bytes: 2 x moved retained    */
+  uint64_t h2d_bytes, d2h_bytes, scatter_bytes;
+  int32_t n_launches;
+  int32_t reserved;
+} atp_timing;
+
+/* Wait for the pending reshard calls of `plan`; returns the first
+ * asynchronous error (ATP_EINVAL for a bad block table, ATP_EHIP).
+ * `out` may be NULL. */
+int atp_sync(atp_plan_t *plan, atp_timing *out);
+
+/* ---- inspection helpers (tests, benchmark) ------------------------------ */
+typedef struct {
+  int32_t self_new_rank;
+  int32_t n_levels_w;   /* in-place levels (1 when out of place)      */
+  int32_t n_levels_kv;
+  int32_t n_desc_w, n_desc_kv;
+  int32_t reserved;
+  uint64_t old_arena_bytes, new_arena_bytes; /* weights, packed layouts */
+  uint64_t old_kv_bytes, new_kv_bytes;
+  uint64_t retained_w, inflow_w, outbound_w; /* this GPU, bytes          */
+  uint64_t retained_kv, inflow_kv, outbound_kv;
+  uint64_t moved_w, moved_kv;   /* retained bytes whose address changes */
+  uint64_t staged_w, staged_kv; /* in place: bytes routed via staging   */
+  uint64_t staging_w, staging_kv; /* staging bytes each call needs      */
+  uint64_t global_keep, global_p2p, global_reload; /* all survivors     */
+  uint64_t reload_min;          /* Eq. 1, bytes                         */
+} atp_stats;
+int atp_plan_stats(const atp_plan_t *plan, atp_stats *out);
+
+enum { ATP_KEEP = 0, ATP_P2P = 1, ATP_RELOAD = 2 };
+typedef struct {
+  int32_t kind;     /* ATP_KEEP / ATP_P2P / ATP_RELOAD                   */
+  int32_t src;      /* old rank holding the units, -1 for a reload       */
+  int32_t dst;      /* target index (new rank)                           */
+  int32_t host;     /* old rank hosting the target                       */
+  int64_t begin, end;
+} atp_task;
+/* Tasks of one space in plan order (Alg. 1). */
+int atp_plan_tasks(const atp_plan_t *plan, int32_t space, atp_task *out,
+                   int32_t cap, int32_t *n);
+/* Resolved new ranges of one space, in target order. */
+int atp_plan_ranges(const atp_plan_t *plan, int32_t space, atp_range *out,
+                    int32_t cap, int32_t *n);
+/* owner[j] = old rank hosting target j. */
+int atp_plan_owner(const atp_plan_t *plan, int32_t *owner, int32_t cap, int32_t *n);
+/* Old/new byte offsets and new shard bytes of tensor `t`. */
+int atp_plan_layout(const atp_plan_t *plan, int32_t t, uint64_t *old_offset,
+                    uint64_t *new_offset, uint64_t *new_bytes);
+
+/* Packed host-buffer segments, in buffer order. */
+enum { ATP_SEG_INFLOW_W = 0, ATP_SEG_OUTBOUND_W = 1, ATP_SEG_INFLOW_KV = 2,
+       ATP_SEG_OUTBOUND_KV = 3 };
+typedef struct {
+  int32_t tensor;      /* tensor index, or -1 for KV                      */
+  int32_t layer;       /* KV: layer                                       */
+  int32_t which;       /* KV: 0 = K, 1 = V                                */
+  int32_t kind;        /* ATP_P2P / ATP_RELOAD (inflow), ATP_P2P (outbound)*/
+  int64_t unit_begin, unit_end; /* units of the tensor's / KV space      */
+  uint64_t host_offset, bytes;  /* position in the packed host buffer   */
+} atp_segment;
+int atp_plan_segments(const atp_plan_t *plan, int32_t which, atp_segment *out,
+                      int32_t cap, int32_t *n);
+
+/* One kernel launch of the last reshard: kind 0 = weight repack,
+ * 1 = KV repack, 2 = scatter, 3 = staging copy; `ms` from HIP events on
+ * the compute stream. */
+typedef struct {
+  int32_t kind, level;
+  uint64_t bytes;
+  double ms;
+} atp_launch;
+int atp_plan_launches(const atp_plan_t *plan, atp_launch *out, int32_t cap, int32_t *n);
+
+/* The executable schedule of one call (which = 0 weights, 1 KV), in the
+ * order the executor issues it, for replay on a host copy (tests):
+ *   REPACK   device copy of level `level`; all copies of one level run
+ *            concurrently, levels run in order
+ *   H2D_RING host inflow -> landing-ring slot (staging), then the SCATTER
+ *            copies that follow it; ring traffic starts after all levels
+ *   H2D      host inflow -> arena, allowed once level `level` has
+ *            finished (level -1: at any time)
+ *   D2H      arena or staging -> host outbound buffer; must finish
+ *            before level `level` starts (-1: before any inflow landing
+ *            that waits for it); issued one after another in list order
+ *            (in place only)
+ * A copy moves, for each item o in [item_begin, item_end) and line t in
+ * [0, rows), `run` bytes from src_off + i(o) * src_stride + t * src_pitch
+ * to dst_off + j(o) * dst_stride + t * dst_pitch, where i(o) / j(o) is
+ * o - item_begin on a plain side and the o-th live block id (ascending)
+ * on an indexed side; with ATP_COPY_BLOCK_RANGE the items are the live
+ * blocks whose ids lie in [item_begin, item_end). */
+enum { ATP_COPY_REPACK = 0, ATP_COPY_SCATTER = 1, ATP_COPY_H2D = 2, ATP_COPY_H2D_RING = 3,
+       ATP_COPY_D2H = 4 };
+enum { ATP_BUF_OLD = 0, ATP_BUF_NEW = 1, ATP_BUF_STAGING = 2, ATP_BUF_INFLOW = 3,
+       ATP_BUF_OUTBOUND = 4 };
+enum { ATP_COPY_SRC_INDEXED = 1, ATP_COPY_DST_INDEXED = 2, ATP_COPY_BLOCK_RANGE = 4 };
+typedef struct {
+  int32_t op, level;
+  int32_t src_buf, dst_buf;
+  int32_t flags;
+  int32_t after_d2h; /* H2D: the first after_d2h D2H copies of this list
+                        (issued in list order) must have finished      */
+  uint64_t src_off, dst_off, src_pitch, dst_pitch, src_stride, dst_stride;
+  int64_t item_begin, item_end;
+  uint64_t run, rows;
+} atp_copy;
+int atp_plan_copies(const atp_plan_t *plan, int32_t which, atp_copy *out, int32_t cap, int32_t *n);
+
+/* Ranges of a partition of `total` units into `parts` (FLOOR or
+ * CEIL_FIRST). */
+int atp_partition(int64_t total, int32_t parts, int32_t rule, atp_range *out);
+
+const char *atp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ATP_H */

@@ -289,6 +289,49 @@ def kv_live_mask(pb: Problem, table, pool: int, which: str) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
+# packed-buffer segment lists (the packing order stated in the docstring)
+# ----------------------------------------------------------------------------
+def inflow_segments(pb: Problem, n_live: int):
+    """[(tensor index or -1, layer, 0=K/1=V, kind, unit_begin, unit_end,
+    host_offset, bytes)] of the packed inflow buffers (weights, then KV)."""
+    w, at = [], 0
+    for ti, t in enumerate(pb.tensors):
+        ub = t.unit_bytes(pb.eb)
+        for x in _self_tasks(pb, t.space):
+            if x.kind != cmm.KEEP:
+                n = (x.end - x.begin) * ub
+                w.append((ti, t.layer, 0, x.kind, x.begin, x.end, at, n))
+                at += n
+    k, at = [], 0
+    per_head = n_live * pb.block_tokens * pb.head_dim * pb.eb
+    for l in range(pb.n_layers):
+        for which in (0, 1):
+            for x in _self_tasks(pb, pb.kv_space):
+                if x.kind != cmm.KEEP:
+                    n = (x.end - x.begin) * per_head
+                    k.append((-1, l, which, x.kind, x.begin, x.end, at, n))
+                    at += n
+    return w, k
+
+
+def outbound_segments(pb: Problem, n_live: int):
+    w, at = [], 0
+    for ti, t in enumerate(pb.tensors):
+        ub = t.unit_bytes(pb.eb)
+        for a, b in _outbound_pieces(pb, t.space):
+            w.append((ti, t.layer, 0, cmm.P2P, a, b, at, (b - a) * ub))
+            at += (b - a) * ub
+    k, at = [], 0
+    per_head = n_live * pb.block_tokens * pb.head_dim * pb.eb
+    for l in range(pb.n_layers):
+        for which in (0, 1):
+            for a, b in _outbound_pieces(pb, pb.kv_space):
+                k.append((-1, l, which, cmm.P2P, a, b, at, (b - a) * per_head))
+                at += (b - a) * per_head
+    return w, k
+
+
+# ----------------------------------------------------------------------------
 # byte accounting of this GPU's share (definition-level)
 # ----------------------------------------------------------------------------
 def self_bytes(pb: Problem, n_live: int):

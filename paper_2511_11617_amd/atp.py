@@ -1,0 +1,222 @@
+"""ctypes binding of libatp.so (include/atp.h), argument marshalling only.
+
+Every step of the reshard runs in the library: planning on the host in
+C++, repacking and landing in HIP kernels and HIP copies.  Device and
+pinned host buffers are passed as integer addresses (for example
+`tensor.data_ptr()`), streams as `torch.cuda.Stream().cuda_stream`.
+There is no fallback: if the library is missing, importing this module
+raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libatp.so")
+
+# ---- status codes and enums (atp.h) -----------------------------------------
+OK, EINVAL, ECAPACITY, EHIP, EALIGN, ESTATE = 0, -1, -2, -3, -4, -5
+RULE_EXPLICIT, RULE_FLOOR, RULE_CEIL_FIRST, RULE_GQA = 0, 1, 2, 3
+ROWS, COLS = 0, 1
+OFFSET_AUTO = (1 << 64) - 1
+KV_HEAD_MAJOR, KV_TOKEN_MAJOR = 0, 1
+ASSIGN_INORDER, ASSIGN_MAXRETAIN = 0, 1
+INPLACE = 1 << 4
+PLAN_GREEDY = 1 << 8
+PLAN_FULL = 1 << 9
+KEEP, P2P, RELOAD = 0, 1, 2
+SEG_INFLOW_W, SEG_OUTBOUND_W, SEG_INFLOW_KV, SEG_OUTBOUND_KV = 0, 1, 2, 3
+
+EXPORTS = [
+    "atp_plan", "atp_plan_free", "atp_reshard_weights", "atp_reshard_kv", "atp_sync",
+    "atp_plan_stats", "atp_plan_tasks", "atp_plan_ranges", "atp_plan_owner",
+    "atp_plan_layout", "atp_plan_segments", "atp_plan_launches", "atp_partition",
+    "atp_last_error",
+]
+
+
+class Range(C.Structure):
+    _fields_ = [("begin", C.c_int64), ("end", C.c_int64)]
+
+
+class Space(C.Structure):
+    _fields_ = [("total_units", C.c_int64), ("old_tp", C.c_int32), ("new_tp", C.c_int32),
+                ("old_ranges", C.POINTER(Range)), ("new_rule", C.c_int32),
+                ("gqa_space", C.c_int32), ("gqa_group", C.c_int32), ("reserved", C.c_int32),
+                ("new_ranges", C.POINTER(Range))]
+
+
+class Tensor(C.Structure):
+    _fields_ = [("space", C.c_int32), ("kind", C.c_int32), ("layer", C.c_int32),
+                ("elem_bytes", C.c_int32), ("rows", C.c_int64), ("cols", C.c_int64),
+                ("unit", C.c_int64), ("old_offset", C.c_uint64)]
+
+
+class KV(C.Structure):
+    _fields_ = [("space", C.c_int32), ("num_layers", C.c_int32), ("block_tokens", C.c_int32),
+                ("head_dim", C.c_int32), ("elem_bytes", C.c_int32), ("layout", C.c_int32),
+                ("num_blocks", C.c_int64), ("live_blocks", C.c_int64)]
+
+
+class Problem(C.Structure):
+    _fields_ = [("n_spaces", C.c_int32), ("spaces", C.POINTER(Space)),
+                ("n_tensors", C.c_int32), ("tensors", C.POINTER(Tensor)),
+                ("kv", C.POINTER(KV)), ("failed", C.POINTER(C.c_int32)),
+                ("n_failed", C.c_int32), ("self_old_rank", C.c_int32),
+                ("flags", C.c_int32), ("reserved", C.c_int32), ("staging_cap", C.c_uint64)]
+
+
+class Timing(C.Structure):
+    _fields_ = [("plan_ms", C.c_double), ("wall_ms", C.c_double), ("repack_w_ms", C.c_double),
+                ("repack_kv_ms", C.c_double), ("h2d_ms", C.c_double), ("d2h_ms", C.c_double),
+                ("scatter_ms", C.c_double), ("overlap", C.c_double), ("repack_bytes", C.c_uint64),
+                ("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("scatter_bytes", C.c_uint64),
+                ("n_launches", C.c_int32), ("reserved", C.c_int32)]
+
+
+class Stats(C.Structure):
+    _fields_ = [("self_new_rank", C.c_int32), ("n_levels_w", C.c_int32), ("n_levels_kv", C.c_int32),
+                ("n_desc_w", C.c_int32), ("n_desc_kv", C.c_int32), ("reserved", C.c_int32)] + [
+        (n, C.c_uint64) for n in (
+            "old_arena_bytes", "new_arena_bytes", "old_kv_bytes", "new_kv_bytes",
+            "retained_w", "inflow_w", "outbound_w", "retained_kv", "inflow_kv", "outbound_kv",
+            "moved_w", "moved_kv", "staged_w", "staged_kv", "staging_w", "staging_kv",
+            "global_keep", "global_p2p", "global_reload", "reload_min")]
+
+
+class Task(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("src", C.c_int32), ("dst", C.c_int32), ("host", C.c_int32),
+                ("begin", C.c_int64), ("end", C.c_int64)]
+
+
+class Segment(C.Structure):
+    _fields_ = [("tensor", C.c_int32), ("layer", C.c_int32), ("which", C.c_int32),
+                ("kind", C.c_int32), ("unit_begin", C.c_int64), ("unit_end", C.c_int64),
+                ("host_offset", C.c_uint64), ("bytes", C.c_uint64)]
+
+
+class Launch(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("level", C.c_int32), ("bytes", C.c_uint64), ("ms", C.c_double)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2511_11617_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    P = C.c_void_p
+    lib.atp_plan.argtypes = [C.POINTER(Problem), C.POINTER(P)]
+    lib.atp_plan_free.argtypes = [P]
+    lib.atp_plan_free.restype = None
+    lib.atp_reshard_weights.argtypes = [P, P, C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, C.c_uint64,
+                                        P, C.c_uint64, P, P]
+    lib.atp_reshard_kv.argtypes = [P, P, C.c_uint64, P, C.c_uint64, P, C.c_int32, C.c_int32, P,
+                                   C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, P]
+    lib.atp_sync.argtypes = [P, C.POINTER(Timing)]
+    lib.atp_plan_stats.argtypes = [P, C.POINTER(Stats)]
+    lib.atp_plan_tasks.argtypes = [P, C.c_int32, C.POINTER(Task), C.c_int32, C.POINTER(C.c_int32)]
+    lib.atp_plan_ranges.argtypes = [P, C.c_int32, C.POINTER(Range), C.c_int32, C.POINTER(C.c_int32)]
+    lib.atp_plan_owner.argtypes = [P, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32)]
+    lib.atp_plan_layout.argtypes = [P, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+                                    C.POINTER(C.c_uint64)]
+    lib.atp_plan_segments.argtypes = [P, C.c_int32, C.POINTER(Segment), C.c_int32, C.POINTER(C.c_int32)]
+    lib.atp_plan_launches.argtypes = [P, C.POINTER(Launch), C.c_int32, C.POINTER(C.c_int32)]
+    lib.atp_partition.argtypes = [C.c_int64, C.c_int32, C.c_int32, C.POINTER(Range)]
+    lib.atp_last_error.restype = C.c_char_p
+    for f in EXPORTS:
+        getattr(lib, f).restype = getattr(lib, f).restype if f in ("atp_plan_free", "atp_last_error") else C.c_int
+    return lib
+
+
+lib = _load()
+
+
+class AtpError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"atp error {code}: {msg}")
+        self.code = code
+
+
+def _check(rc):
+    if rc != OK:
+        raise AtpError(rc, lib.atp_last_error().decode())
+    return rc
+
+
+def partition(total: int, parts: int, rule: int):
+    out = (Range * parts)()
+    _check(lib.atp_partition(total, parts, rule, out))
+    return [(r.begin, r.end) for r in out]
+
+
+def _list(fn, plan, typ, *args):
+    n = C.c_int32()
+    _check(fn(plan, *args, None, 0, C.byref(n)))
+    arr = (typ * max(n.value, 1))()
+    _check(fn(plan, *args, arr, n.value, C.byref(n)))
+    return list(arr[:n.value])
+
+
+class Plan:
+    """An atp_plan_t and the ctypes objects its problem points into."""
+
+    def __init__(self, problem: Problem, keep=()):
+        self._keep = keep  # arrays referenced by `problem`
+        h = C.c_void_p()
+        _check(lib.atp_plan(C.byref(problem), C.byref(h)))
+        self.h = h
+
+    def close(self):
+        if self.h:
+            lib.atp_plan_free(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def stats(self) -> Stats:
+        s = Stats()
+        _check(lib.atp_plan_stats(self.h, C.byref(s)))
+        return s
+
+    def tasks(self, space: int):
+        return [(t.kind, t.begin, t.end, t.src, t.dst, t.host)
+                for t in _list(lib.atp_plan_tasks, self.h, Task, space)]
+
+    def ranges(self, space: int):
+        return [(r.begin, r.end) for r in _list(lib.atp_plan_ranges, self.h, Range, space)]
+
+    def owner(self):
+        return [int(x) for x in _list(lib.atp_plan_owner, self.h, C.c_int32)]
+
+    def layout(self, t: int):
+        o, n, b = C.c_uint64(), C.c_uint64(), C.c_uint64()
+        _check(lib.atp_plan_layout(self.h, t, C.byref(o), C.byref(n), C.byref(b)))
+        return o.value, n.value, b.value
+
+    def segments(self, which: int):
+        return _list(lib.atp_plan_segments, self.h, Segment, which)
+
+    def launches(self):
+        return _list(lib.atp_plan_launches, self.h, Launch)
+
+    def reshard_weights(self, arena, arena_bytes, new_arena, new_bytes, inflow, inflow_bytes,
+                        outbound, outbound_bytes, staging, staging_bytes, compute, copy):
+        _check(lib.atp_reshard_weights(self.h, arena, arena_bytes, new_arena, new_bytes, inflow,
+                                       inflow_bytes, outbound, outbound_bytes, staging,
+                                       staging_bytes, compute, copy))
+
+    def reshard_kv(self, arena, arena_bytes, new_arena, new_bytes, table, n_seq, max_blocks,
+                   inflow, inflow_bytes, outbound, outbound_bytes, staging, staging_bytes,
+                   compute, copy):
+        _check(lib.atp_reshard_kv(self.h, arena, arena_bytes, new_arena, new_bytes, table, n_seq,
+                                  max_blocks, inflow, inflow_bytes, outbound, outbound_bytes,
+                                  staging, staging_bytes, compute, copy))
+
+    def sync(self) -> Timing:
+        t = Timing()
+        _check(lib.atp_sync(self.h, C.byref(t)))
+        return t

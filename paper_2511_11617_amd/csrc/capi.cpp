@@ -1,0 +1,259 @@
+// capi.cpp — the extern "C" boundary of the reshard library: argument
+// marshalling, error codes and the thread-local error message.  All work
+// happens in plan.cpp (host planning) and exec.hip (GPU execution).
+#include <algorithm>
+#include <climits>
+#include <cstring>
+#include <string>
+
+#include "../../include/atp.h"
+#include "exec.h"
+#include "plan.h"
+
+struct atp_plan_obj {
+  atp::Plan *p;
+};
+
+namespace {
+thread_local std::string g_err;
+
+int fail(int code, const std::string &m) {
+  g_err = m;
+  return code;
+}
+
+template <class F>
+int guard(F &&f) {
+  try {
+    return f();
+  } catch (const atp::Error &e) {
+    return fail(e.code, e.what());
+  } catch (const std::bad_alloc &) {
+    return fail(ATP_ECAPACITY, "host allocation failed");
+  } catch (const std::exception &e) {
+    return fail(ATP_EINVAL, e.what());
+  }
+}
+
+template <class T, class Src>
+int copy_out(const Src &src, T *out, int32_t cap, int32_t *n) {
+  if (!n) return fail(ATP_EINVAL, "n is NULL");
+  *n = int32_t(src.size());
+  if (out) {
+    if (cap < *n) return fail(ATP_ECAPACITY, "output array too small");
+    for (size_t i = 0; i < src.size(); ++i) out[i] = src[i];
+  }
+  return ATP_OK;
+}
+}  // namespace
+
+extern "C" {
+
+const char *atp_last_error(void) { return g_err.c_str(); }
+
+int atp_plan(const atp_problem *problem, atp_plan_t **out) {
+  return guard([&]() -> int {
+    if (!out) return fail(ATP_EINVAL, "out is NULL");
+    atp::Plan *p = atp::make_plan(problem);
+    *out = new atp_plan_obj{p};
+    return ATP_OK;
+  });
+}
+
+void atp_plan_free(atp_plan_t *plan) {
+  if (!plan) return;
+  try {
+    atp::exec_free(*plan->p);
+  } catch (...) {
+  }
+  delete plan->p;
+  delete plan;
+}
+
+int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes, void *new_arena,
+                        uint64_t new_arena_bytes, const void *inflow_host, uint64_t inflow_bytes,
+                        void *outbound_host, uint64_t outbound_bytes, void *staging, uint64_t staging_bytes,
+                        atp_stream compute, atp_stream copy) {
+  return guard([&]() -> int {
+    if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+    atp::exec_call(*plan->p, false, arena, arena_bytes, new_arena, new_arena_bytes, inflow_host, inflow_bytes,
+                   outbound_host, outbound_bytes, nullptr, 0, staging, staging_bytes,
+                   static_cast<hipStream_t>(compute), static_cast<hipStream_t>(copy));
+    return ATP_OK;
+  });
+}
+
+int atp_reshard_kv(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes, void *new_kv_arena, uint64_t new_kv_bytes,
+                   const int32_t *block_table, int32_t n_seq, int32_t max_blocks, const void *inflow_host,
+                   uint64_t inflow_bytes, void *outbound_host, uint64_t outbound_bytes, void *staging,
+                   uint64_t staging_bytes, atp_stream compute, atp_stream copy) {
+  return guard([&]() -> int {
+    if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+    if (!plan->p->has_kv) return fail(ATP_EINVAL, "the problem has no KV cache");
+    if (n_seq <= 0 || max_blocks <= 0) return fail(ATP_EINVAL, "block table must have positive size");
+    atp::exec_call(*plan->p, true, kv_arena, kv_bytes, new_kv_arena, new_kv_bytes, inflow_host, inflow_bytes,
+                   outbound_host, outbound_bytes, block_table, int64_t(n_seq) * max_blocks, staging, staging_bytes,
+                   static_cast<hipStream_t>(compute), static_cast<hipStream_t>(copy));
+    return ATP_OK;
+  });
+}
+
+int atp_sync(atp_plan_t *plan, atp_timing *out) {
+  return guard([&]() -> int {
+    if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+    return atp::exec_sync(*plan->p, out);
+  });
+}
+
+int atp_plan_stats(const atp_plan_t *plan, atp_stats *out) {
+  if (!plan || !out) return fail(ATP_EINVAL, "NULL argument");
+  *out = plan->p->stats;
+  return ATP_OK;
+}
+
+int atp_plan_tasks(const atp_plan_t *plan, int32_t space, atp_task *out, int32_t cap, int32_t *n) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  if (space < 0 || space >= int32_t(plan->p->sp.size())) return fail(ATP_EINVAL, "bad space");
+  return copy_out(plan->p->sp[space].tasks, out, cap, n);
+}
+
+int atp_plan_ranges(const atp_plan_t *plan, int32_t space, atp_range *out, int32_t cap, int32_t *n) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  if (space < 0 || space >= int32_t(plan->p->sp.size())) return fail(ATP_EINVAL, "bad space");
+  std::vector<atp_range> r;
+  for (const atp::Rng &x : plan->p->sp[space].new_r) r.push_back({x.b, x.e});
+  return copy_out(r, out, cap, n);
+}
+
+int atp_plan_owner(const atp_plan_t *plan, int32_t *owner, int32_t cap, int32_t *n) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  std::vector<int32_t> o(plan->p->owner.begin(), plan->p->owner.end());
+  return copy_out(o, owner, cap, n);
+}
+
+int atp_plan_layout(const atp_plan_t *plan, int32_t t, uint64_t *old_offset, uint64_t *new_offset,
+                    uint64_t *new_bytes) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  if (t < 0 || t >= int32_t(plan->p->tp.size())) return fail(ATP_EINVAL, "bad tensor index");
+  const atp::TensorPlan &tp = plan->p->tp[t];
+  if (old_offset) *old_offset = tp.old_off;
+  if (new_offset) *new_offset = tp.new_off;
+  if (new_bytes) *new_bytes = tp.new_bytes;
+  return ATP_OK;
+}
+
+int atp_plan_segments(const atp_plan_t *plan, int32_t which, atp_segment *out, int32_t cap, int32_t *n) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  const atp::Plan &P = *plan->p;
+  switch (which) {
+    case ATP_SEG_INFLOW_W: return copy_out(P.w.seg_in, out, cap, n);
+    case ATP_SEG_OUTBOUND_W: return copy_out(P.w.seg_out, out, cap, n);
+    case ATP_SEG_INFLOW_KV: return copy_out(P.k.seg_in, out, cap, n);
+    case ATP_SEG_OUTBOUND_KV: return copy_out(P.k.seg_out, out, cap, n);
+    default: return fail(ATP_EINVAL, "bad segment kind");
+  }
+}
+
+int atp_plan_launches(const atp_plan_t *plan, atp_launch *out, int32_t cap, int32_t *n) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  std::vector<atp_launch> v;
+  atp::exec_launches(*plan->p, v);
+  return copy_out(v, out, cap, n);
+}
+
+int atp_plan_copies(const atp_plan_t *plan, int32_t which, atp_copy *out, int32_t cap, int32_t *n) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  const atp::Plan &P = *plan->p;
+  if (which != 0 && which != 1) return fail(ATP_EINVAL, "which must be 0 (weights) or 1 (KV)");
+  const atp::CallPlan &c = which ? P.k : P.w;
+  auto buf_of = [&](uint32_t slot) {
+    if (slot == atp::BUF_STAGE) return int32_t(ATP_BUF_STAGING);
+    if (slot == atp::BUF_OUT) return int32_t(P.inplace ? ATP_BUF_OLD : ATP_BUF_NEW);
+    return int32_t(ATP_BUF_OLD);
+  };
+  auto dev_copy = [&](const atp::Fam &f, int op, int level) {
+    atp_copy x{};
+    x.op = op;
+    x.level = level;
+    x.src_buf = buf_of((f.flags >> atp::DF_SRC_SHIFT) & 3);
+    x.dst_buf = buf_of((f.flags >> atp::DF_DST_SHIFT) & 3);
+    x.flags = ((f.flags & atp::DF_SRC_IND) ? ATP_COPY_SRC_INDEXED : 0) |
+              ((f.flags & atp::DF_DST_IND) ? ATP_COPY_DST_INDEXED : 0) |
+              ((f.flags & atp::DF_BLOCKRANGE) ? ATP_COPY_BLOCK_RANGE : 0);
+    x.src_off = f.src_off;
+    x.dst_off = f.dst_off;
+    x.src_pitch = f.src_pitch;
+    x.dst_pitch = f.dst_pitch;
+    x.src_stride = f.src_ostride;
+    x.dst_stride = f.dst_ostride;
+    x.item_begin = f.o_begin;
+    x.item_end = f.o_end;
+    x.run = f.run;
+    x.rows = f.rows;
+    return x;
+  };
+  auto host_copy = [&](const atp::HostCopy &h, int op, int level, bool to_host) {
+    atp_copy x{};
+    x.op = op;
+    x.level = level;
+    int32_t dev = h.dev_buf == atp::BUF_STAGE ? int32_t(ATP_BUF_STAGING) : buf_of(uint32_t(h.dev_buf));
+    x.src_buf = to_host ? dev : int32_t(ATP_BUF_INFLOW);
+    x.dst_buf = to_host ? int32_t(ATP_BUF_OUTBOUND) : dev;
+    x.src_off = to_host ? h.dev_off : h.host_off;
+    x.dst_off = to_host ? h.host_off : h.dev_off;
+    uint64_t run = h.rows > 1 ? h.run : h.bytes;
+    x.src_stride = to_host ? h.dev_pitch : run;
+    x.dst_stride = to_host ? run : run;
+    x.item_begin = 0;
+    x.item_end = int64_t(h.rows > 1 ? h.rows : 1);
+    x.run = run;
+    x.rows = 1;
+    return x;
+  };
+  std::vector<atp_copy> v;
+  // outbound reads first, in the order the executor issues them (by the
+  // level that needs them); each must finish before that level
+  std::vector<int> pos(c.outbound.size(), -1);
+  if (P.inplace) {
+    std::vector<int> need(c.outbound.size(), INT32_MAX);
+    for (const atp::Launch &L : c.levels)
+      for (int o : L.wait_outbound) need[o] = std::min(need[o], L.level);
+    std::vector<int> ord;
+    for (size_t o = 0; o < c.outbound.size(); ++o)
+      if (c.outbound[o].dev_buf != atp::BUF_STAGE) ord.push_back(int(o));
+    std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return need[a] < need[b]; });
+    for (size_t k = 0; k < ord.size(); ++k) {
+      int o = ord[k];
+      pos[o] = int(k);
+      v.push_back(host_copy(c.outbound[o], ATP_COPY_D2H, need[o] == INT32_MAX ? -1 : need[o], true));
+    }
+  }
+  for (const atp::Launch &L : c.levels)
+    for (int d = L.d0; d < L.d1; ++d) v.push_back(dev_copy(c.fams[d], ATP_COPY_REPACK, L.level));
+  if (P.inplace)  // outbound gathered into staging at level 0 (KV)
+    for (const atp::HostCopy &h : c.outbound)
+      if (h.dev_buf == atp::BUF_STAGE) v.push_back(host_copy(h, ATP_COPY_D2H, 1, true));
+  for (const atp::HostCopy &h : c.directs) {
+    atp_copy x = host_copy(h, ATP_COPY_H2D, h.gate_level, false);
+    for (int o : h.gate_out) x.after_d2h = std::max(x.after_d2h, pos[o] + 1);
+    v.push_back(x);
+  }
+  for (const atp::Chunk &ch : c.chunks) {
+    for (const atp::HostCopy &h : ch.copies) v.push_back(host_copy(h, ATP_COPY_H2D_RING, -1, false));
+    for (const atp::Launch &L : ch.scatters)
+      for (int d = L.d0; d < L.d1; ++d) v.push_back(dev_copy(c.fams[d], ATP_COPY_SCATTER, -1));
+  }
+  return copy_out(v, out, cap, n);
+}
+
+int atp_partition(int64_t total, int32_t parts, int32_t rule, atp_range *out) {
+  return guard([&]() -> int {
+    if (!out) return fail(ATP_EINVAL, "out is NULL");
+    std::vector<atp::Rng> r;
+    atp::partition(total, parts, rule, r);
+    for (int i = 0; i < parts; ++i) out[i] = {r[i].b, r[i].e};
+    return ATP_OK;
+  });
+}
+
+}  // extern "C"

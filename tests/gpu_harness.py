@@ -1,0 +1,121 @@
+"""Run one reshard through the C ABI on the GPU and check it against the
+oracle (shared helper of the GPU tests).
+
+Inputs and expected bytes come from the oracle (plain CPU definition) and
+the seeded generator; the library only sees the old arena, the packed
+inflow buffer and the block table.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import model, repack
+from paper_2511_11617_amd import atp, problem
+from synth import pagetable
+from synth.content import Content
+
+POISON = 0xA5
+
+
+class CachedContent:
+    """Memoises full-tensor requests (idx = arange(n)) of a Content."""
+
+    def __init__(self, content):
+        self.c = content
+        self.cache = {}
+
+    def __call__(self, tag, layer, idx):
+        n = len(idx)
+        if n and idx[0] == 0 and idx[-1] == n - 1:
+            k = (tag, layer, n)
+            if k not in self.cache:
+                self.cache[k] = self.c(tag, layer, idx)
+            return self.cache[k]
+        return self.c(tag, layer, idx)
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name=""):
+    say(f"[gpu case] {name} cfg={c.get('name', '?')} layers={c['layers']} flags={flags} "
+        f"old_tp={c['old_tp']} new_tp={c['new_tp']} failed={c['failed']} self_old={c['self_old']}")
+    pb = model.build(c, assign=assign)
+    content = CachedContent(Content(c["seed"], c["w_kind"], c["kv_kind"]))
+    table, pool = pagetable.make_for(c)
+    n_live = int(len(repack.live_blocks(table)))
+    inplace = bool(flags & atp.INPLACE)
+
+    old_w = repack.weight_arena(pb, content, "old")
+    want_w = repack.weight_arena(pb, content, "new")
+    mask_w = repack.weight_live_mask(pb, "new")
+    in_w = repack.packed_weight_inflow(pb, content)
+    old_k = repack.kv_arena(pb, content, table, pool, "old", poison=0xDEAD)
+    want_k = repack.kv_arena(pb, content, table, pool, "new")
+    mask_k = repack.kv_live_mask(pb, table, pool, "new")
+    in_k = repack.packed_kv_inflow(pb, content, table, pool)
+
+    b = problem.build(c, n_live=n_live, pool=pool, flags=flags, staging_cap=staging_cap)
+    plan = b.plan()
+    st = plan.stats()
+    assert st.inflow_w == in_w.size and st.inflow_kv == in_k.size
+
+    dev = torch.device("cuda")
+    u8 = torch.uint8
+
+    def device_arena(old, new_size):
+        if inplace:
+            a = torch.full((max(old.size, new_size, 256),), POISON, dtype=u8, device=dev)
+            a[:old.size].copy_(torch.from_numpy(old))
+            return a, None
+        a = torch.from_numpy(old).to(dev) if old.size else torch.zeros(256, dtype=u8, device=dev)
+        n = torch.full((max(new_size, 256),), POISON, dtype=u8, device=dev)
+        return a, n
+
+    def pinned(arr):
+        if arr.size == 0:
+            return None
+        t = torch.empty(arr.size, dtype=u8, pin_memory=True)
+        t.copy_(torch.from_numpy(arr))
+        return t
+
+    aw, nw = device_arena(old_w, want_w.size)
+    ak, nk = device_arena(old_k, want_k.size)
+    stage_w = torch.full((max(st.staging_w, 256),), 0x5A, dtype=u8, device=dev)
+    stage_k = torch.full((max(st.staging_kv, 256),), 0x5A, dtype=u8, device=dev)
+    hin_w, hin_k = pinned(in_w), pinned(in_k)
+    hout_w = torch.full((max(st.outbound_w, 1),), 0x3C, dtype=u8, pin_memory=True)
+    hout_k = torch.full((max(st.outbound_kv, 1),), 0x3C, dtype=u8, pin_memory=True)
+    table_d = torch.from_numpy(table).to(dev)
+    compute = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    ptr = lambda t: t.data_ptr() if t is not None else None
+    plan.reshard_weights(ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0,
+                         ptr(hin_w), in_w.size, ptr(hout_w), st.outbound_w, ptr(stage_w), stage_w.numel(),
+                         compute.cuda_stream, copy.cuda_stream)
+    plan.reshard_kv(ptr(ak), ak.numel(), ptr(nk), nk.numel() if nk is not None else 0,
+                    ptr(table_d), table.shape[0], table.shape[1], ptr(hin_k), in_k.size,
+                    ptr(hout_k), st.outbound_kv, ptr(stage_k), stage_k.numel(),
+                    compute.cuda_stream, copy.cuda_stream)
+    t = plan.sync()
+    torch.cuda.synchronize()
+
+    got_w = (aw if inplace else nw).cpu().numpy()[:want_w.size]
+    got_k = (ak if inplace else nk).cpu().numpy()[:want_k.size]
+    bad_w = np.flatnonzero(got_w[mask_w] != want_w[mask_w])
+    bad_k = np.flatnonzero(got_k[mask_k] != want_k[mask_k])
+    assert bad_w.size == 0, f"weights: {bad_w.size} wrong bytes, first at live byte {bad_w[:5]}"
+    assert bad_k.size == 0, f"kv: {bad_k.size} wrong bytes, first at live byte {bad_k[:5]}"
+    if inplace and check_outbound:
+        ow = repack.packed_weight_outbound(pb, content)
+        ok = repack.packed_kv_outbound(pb, content, table, pool)
+        np.testing.assert_array_equal(hout_w.numpy()[:ow.size], ow)
+        np.testing.assert_array_equal(hout_k.numpy()[:ok.size], ok)
+    return t, plan, st

@@ -1,0 +1,71 @@
+"""Bit-exact parity of the HIP reshard with the oracle (GPU, through the C ABI).
+
+Small cases the oracle materialises in seconds: the tiny 4 -> 3 workload,
+random small decoders (odd sizes, unaligned runs, replicated KV heads,
+fragmented block tables, both KV layouts, 16-bit payloads with NaN / Inf
+/ -0 patterns), the per-layer shapes of the four large workloads with few
+layers and sequences, out of place (destination poisoned first) and in
+place.
+"""
+import random
+
+import pytest
+import torch
+
+from paper_2511_11617_amd import atp
+from synth import configs
+from synth.content import KIND_RAW16, KIND_TAG16
+from tests.gpu_harness import run_case
+from tests.test_oracle_repack import tiny_cfg
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.mark.parametrize("layout", ["head", "token"])
+@pytest.mark.parametrize("payload", ["normal", "raw"])
+def test_cfg1_out_of_place(layout, payload):
+    kw = {"kv_layout": layout}
+    if payload == "raw":
+        kw.update(w_kind=KIND_RAW16, kv_kind=KIND_RAW16)
+    run_case(configs.get(1, **kw), name="cfg1")
+
+
+@pytest.mark.parametrize("self_old", [0, 2, 3])
+def test_cfg1_every_survivor(self_old):
+    run_case(configs.get(1, self_old=self_old), name="cfg1-survivor")
+
+
+@pytest.mark.parametrize("layout", ["head", "token"])
+def test_cfg1_in_place(layout):
+    run_case(configs.get(1, kv_layout=layout), flags=atp.INPLACE, name="cfg1-inplace")
+
+
+@pytest.mark.parametrize("seed", list(range(24)))
+def test_random_small(seed):
+    rng = random.Random(seed)
+    c = tiny_cfg(rng, experts=seed % 3 == 0)
+    run_case(c, name=f"random-{seed}")
+
+
+@pytest.mark.parametrize("seed", list(range(24)))
+def test_random_small_in_place(seed):
+    rng = random.Random(1000 + seed)
+    c = tiny_cfg(rng, experts=seed % 3 == 0)
+    run_case(c, flags=atp.INPLACE, name=f"random-inplace-{seed}")
+
+
+@pytest.mark.parametrize("n", [2, 3, 4])
+def test_large_shapes_one_layer(n):
+    c = configs.scaled(n, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    run_case(c, name=f"cfg{n}-1layer")
+
+
+def test_cfg5_shape_in_place_two_layers():
+    c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    run_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"], name="cfg5-2layers-inplace")

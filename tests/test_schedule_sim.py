@@ -1,0 +1,93 @@
+"""Replay the library's schedule on the host and compare with the oracle (CPU).
+
+Catches out-of-bounds descriptors, in-place ordering hazards (a level that
+reads bytes it or a sibling overwrites, inflow landing on bytes a later
+level still reads, outbound reads after an overwrite) and wrong addresses,
+before anything runs on a GPU.
+"""
+import random
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import model, repack
+from paper_2511_11617_amd import atp, problem
+from synth import configs, pagetable
+from synth.content import KIND_TAG16, Content
+from tests.gpu_harness import CachedContent
+from tests.schedule_sim import INFLOW, NEW, OLD, OUTBOUND, STAGING, copies, replay
+from tests.test_oracle_repack import tiny_cfg
+
+
+def sim_case(c, flags=0, staging_cap=0, assign="inorder"):
+    pb = model.build(c, assign=assign)
+    content = CachedContent(Content(c["seed"], c["w_kind"], c["kv_kind"]))
+    table, pool = pagetable.make_for(c)
+    live = repack.live_blocks(table)
+    inplace = bool(flags & atp.INPLACE)
+    b = problem.build(c, n_live=len(live), pool=pool, flags=flags, staging_cap=staging_cap)
+    plan = b.plan()
+    st_ = plan.stats()
+    # weights, then KV
+    cases = [
+        (0, repack.weight_arena(pb, content, "old"), repack.weight_arena(pb, content, "new"),
+         repack.weight_live_mask(pb, "new"), repack.packed_weight_inflow(pb, content),
+         repack.packed_weight_outbound(pb, content), st_.staging_w),
+        (1, repack.kv_arena(pb, content, table, pool, "old", poison=0xDEAD),
+         repack.kv_arena(pb, content, table, pool, "new"), repack.kv_live_mask(pb, table, pool, "new"),
+         repack.packed_kv_inflow(pb, content, table, pool), repack.packed_kv_outbound(pb, content, table, pool),
+         st_.staging_kv),
+    ]
+    for which, old, want, mask, inflow, outbound, staging in cases:
+        cps = copies(plan, which)
+        n = max(old.size, want.size)
+        bufs = {
+            OLD: np.full(n if inplace else old.size, 0xA5, np.uint8),
+            NEW: np.full(want.size, 0xA5, np.uint8),
+            STAGING: np.full(staging, 0x5A, np.uint8),
+            INFLOW: inflow.copy(),
+            OUTBOUND: np.full(max(outbound.size, 1), 0x3C, np.uint8),
+        }
+        bufs[OLD][:old.size] = old
+        replay(cps, bufs, live)
+        got = (bufs[OLD] if inplace else bufs[NEW])[:want.size]
+        bad = np.flatnonzero(got[mask] != want[mask])
+        assert bad.size == 0, f"{'kv' if which else 'weights'}: {bad.size} wrong bytes"
+        if inplace:
+            np.testing.assert_array_equal(bufs[OUTBOUND][:outbound.size], outbound)
+        else:
+            np.testing.assert_array_equal(bufs[OLD][:old.size], old)  # old arena untouched
+    return plan
+
+
+@pytest.mark.parametrize("inplace", [False, True])
+@pytest.mark.parametrize("layout", ["head", "token"])
+def test_cfg1(inplace, layout):
+    sim_case(configs.get(1, kv_layout=layout, w_kind=KIND_TAG16, kv_kind=KIND_TAG16),
+             flags=atp.INPLACE if inplace else 0)
+
+
+@pytest.mark.parametrize("self_old", [0, 2, 3])
+def test_cfg1_survivors_in_place(self_old):
+    sim_case(configs.get(1, self_old=self_old, w_kind=KIND_TAG16, kv_kind=KIND_TAG16), flags=atp.INPLACE)
+
+
+@settings(max_examples=80, deadline=None)
+@given(st.integers(0, 2 ** 31), st.booleans(), st.booleans())
+def test_random_small(seed, experts, inplace):
+    c = tiny_cfg(random.Random(seed), experts)
+    sim_case(c, flags=atp.INPLACE if inplace else 0)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("n", [2, 3, 4])
+def test_large_shapes_one_layer(n):
+    c = configs.scaled(n, layers=1, n_seq=2, seq_tokens=128, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    sim_case(c)
+
+
+@pytest.mark.slow
+def test_cfg5_shape_in_place_two_layers():
+    c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=128, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    sim_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"])
