@@ -1,0 +1,268 @@
+"""Benchmark of one surviving GPU's share of a TP reshard on MI355X.
+
+A step is the whole hot path once: plan (partitions, CMM tasks, layouts,
+descriptors), repack the retained weight slices and paged-KV head ranges,
+land the missing bytes from pinned host memory on a side stream, sync.
+Inputs are synthetic (seeded generator), resident in HBM and pinned host
+memory before the timed region.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N]
+
+Prints one JSON line.  `value` is the repack throughput in algorithmic
+bytes (one read and one write of every retained byte that moves) per
+second of device repack time; `ms_per_step` is the wall time of a whole
+step, which the PCIe-bound inflow dominates.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=2,
+                    help="1..5; 2 = dense 40L h5120 TP 4->3 (the headline workload)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=2,
+                    help="layers of the workload the CPU oracle is timed on")
+    ap.add_argument("--calib-copy-gib", type=float, default=0.0,
+                    help="also run a plain device copy of this size (counter calibration)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark measures one GPU's share of the reshard; "
+                                   "run it with --gpus 1 (multi-GPU runs are not part of it)"}))
+        sys.exit(2)
+    import torch
+
+    from paper_2511_11617_amd import atp, problem
+    from synth import configs, fill, pagetable
+    from synth.content import TAGS, Content
+
+    cfg = configs.get(args.workload)
+    table, pool = pagetable.make_for(cfg)
+    n_live = int(len(np.unique(table[table >= 0])))
+    inplace = bool(cfg["inplace"])
+    flags = atp.INPLACE if inplace else 0
+    cap = cfg["staging_cap"] or 0
+    built = problem.build(cfg, n_live=n_live, pool=pool, flags=flags, staging_cap=cap)
+    plan = built.plan()
+    st = plan.stats()
+    dev = torch.device("cuda")
+    u8 = torch.uint8
+    content = Content(cfg["seed"], cfg["w_kind"], cfg["kv_kind"])
+    self_old = cfg["self_old"]
+    layout = atp.KV_TOKEN_MAJOR if cfg.get("kv_layout") == "token" else atp.KV_HEAD_MAJOR
+    bt, hd = cfg["block_tokens"], cfg["head_dim"]
+    log(f"[bench] workload {args.workload} {cfg['name']}: R_w={st.retained_w / 1e9:.3f} GB "
+        f"R_kv={st.retained_kv / 1e9:.3f} GB I={(st.inflow_w + st.inflow_kv) / 1e9:.3f} GB "
+        f"levels={st.n_levels_w}/{st.n_levels_kv} inplace={inplace}")
+
+    # ---- buffers ---------------------------------------------------------------
+    def arena(old_b, new_b):
+        if inplace:
+            return torch.empty(max(old_b, new_b, 256), dtype=u8, device=dev), None
+        return (torch.empty(max(old_b, 256), dtype=u8, device=dev),
+                torch.empty(max(new_b, 256), dtype=u8, device=dev))
+
+    aw, nw = arena(st.old_arena_bytes, st.new_arena_bytes)
+    ak, nk = arena(st.old_kv_bytes, st.new_kv_bytes)
+    stage_w = torch.empty(max(st.staging_w, 256), dtype=u8, device=dev)
+    stage_k = torch.empty(max(st.staging_kv, 256), dtype=u8, device=dev)
+    hin_w = torch.empty(max(st.inflow_w, 1), dtype=u8, pin_memory=True)
+    hin_k = torch.empty(max(st.inflow_kv, 1), dtype=u8, pin_memory=True)
+    hout_w = torch.empty(max(st.outbound_w if inplace else 1, 1), dtype=u8, pin_memory=True)
+    hout_k = torch.empty(max(st.outbound_kv if inplace else 1, 1), dtype=u8, pin_memory=True)
+    table_d = torch.from_numpy(table).to(dev)
+
+    # ---- synthetic content -----------------------------------------------------
+    t0 = time.time()
+    tl = built.tensors
+    old_r = built.old_ranges
+
+    def fill_old():
+        shards = []
+        for i, (name, l, kind, sp, rows, cols, unit) in enumerate(tl):
+            a, b = old_r[sp][self_old]
+            shards.append((TAGS[name], l, kind == atp.ROWS, rows, cols, unit, a, b, plan.layout(i)[0]))
+        fill.weights(aw, content, shards)
+        fill.kv_arena(ak, content, table, pool, cfg["layers"], old_r[1][self_old], cfg["n_kv"],
+                      cfg["seq_tokens"], bt, hd, layout)
+
+    fill_old()
+    tmp = torch.empty(max(st.inflow_w, st.inflow_kv, 1), dtype=u8, device=dev)
+    shards = []
+    for s in plan.segments(atp.SEG_INFLOW_W):
+        name, l, kind, sp, rows, cols, unit = tl[s.tensor]
+        shards.append((TAGS[name], l, kind == atp.ROWS, rows, cols, unit, s.unit_begin, s.unit_end,
+                       s.host_offset))
+    fill.weights(tmp, content, shards)
+    hin_w.copy_(tmp[:hin_w.numel()])
+    segs = [(s.layer, s.which, s.unit_begin, s.unit_end, s.host_offset)
+            for s in plan.segments(atp.SEG_INFLOW_KV)]
+    fill.kv_packed(tmp, content, table, pool, segs, cfg["n_kv"], cfg["seq_tokens"], bt, hd, layout)
+    hin_k.copy_(tmp[:hin_k.numel()])
+    del tmp
+    torch.cuda.synchronize()
+    log(f"[bench] inputs generated in {time.time() - t0:.1f} s")
+
+    compute = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    ptr = lambda t: t.data_ptr() if t is not None else None
+
+    def step():
+        p = built.plan()
+        p.reshard_weights(ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0,
+                          ptr(hin_w), st.inflow_w, ptr(hout_w), st.outbound_w if inplace else 0,
+                          ptr(stage_w), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
+        p.reshard_kv(ptr(ak), ak.numel(), ptr(nk), nk.numel() if nk is not None else 0,
+                     ptr(table_d), table.shape[0], table.shape[1], ptr(hin_k), st.inflow_kv,
+                     ptr(hout_k), st.outbound_kv if inplace else 0, ptr(stage_k), stage_k.numel(),
+                     compute.cuda_stream, copy.cuda_stream)
+        t = p.sync()
+        return p, t
+
+    for i in range(args.warmup):
+        if inplace and i:
+            fill_old()
+        step()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    recs, launches = [], []
+    elapsed = 0.0
+    for i in range(args.steps):
+        if inplace:
+            fill_old()  # restore the old layout (untimed)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        p, t = step()
+        torch.cuda.synchronize()
+        elapsed += time.perf_counter() - t1
+        recs.append(t)
+        launches.append([(x.kind, x.level, x.bytes, x.ms) for x in p.launches()])
+        log(f"[bench] step {i + 1}/{args.steps}: wall {t.wall_ms:.1f} ms, repack "
+            f"{t.repack_w_ms + t.repack_kv_ms:.3f} ms, h2d {t.h2d_ms:.1f} ms")
+
+    if args.calib_copy_gib > 0:
+        n = int(args.calib_copy_gib * (1 << 30))
+        src = torch.empty(n, dtype=u8, device=dev)
+        dst = torch.empty(n, dtype=u8, device=dev)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    K = args.steps
+    alg = 2 * (st.moved_w + st.moved_kv)
+    rep_ms = sum(t.repack_w_ms + t.repack_kv_ms for t in recs) / K
+    value = alg / (rep_ms * 1e-3) / 1e9
+    wall_ms = elapsed / K * 1e3
+    h2d_ms = sum(t.h2d_ms for t in recs) / K
+    # dominant kernel: the repack launch moving the most bytes
+    per = {}
+    for L in launches:
+        for kind, level, b, ms in L:
+            if kind in (0, 1):
+                per.setdefault((kind, level, b), []).append(ms)
+    (dk, dl, db), dms = max(per.items(), key=lambda kv: kv[0][2])
+    dom_ms = sum(dms) / len(dms)
+    dom_gbps = 2 * db / (dom_ms * 1e-3) / 1e9
+    kernels = [{"call": "weights" if k == 0 else "kv",
+                "level": l, "alg_bytes": 2 * b, "avg_ms": round(sum(v) / len(v), 4),
+                "GBps": round(2 * b / (sum(v) / len(v) * 1e-3) / 1e9, 1)}
+               for (k, l, b), v in sorted(per.items())][:8]
+
+    out = {
+        "metric": "reshard GB/s (fraction of HBM peak) + wall ms per TP k→k-1; reload bytes vs min",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "layers": cfg["layers"], "hidden": cfg["hidden"],
+                   "tp": f"{cfg['old_tp']}->{cfg['new_tp']}", "failed": cfg["failed"],
+                   "self_old_rank": self_old, "self_new_rank": st.self_new_rank,
+                   "kv_sequences": cfg["n_seq"], "seq_tokens": cfg["seq_tokens"],
+                   "in_place": inplace, "elem": "bf16" if cfg["elem_bytes"] == 2 else "?"},
+        "hbm_frac": round(value / HBM_PEAK_GBPS, 4),
+        "repack_ms": round(rep_ms, 4),
+        "wall_ms": round(wall_ms, 3),
+        "plan_ms": round(sum(t.plan_ms for t in recs) / K, 3),
+        "h2d_GBps_pcie_inclusive": round((st.inflow_w + st.inflow_kv) / (h2d_ms * 1e-3) / 1e9, 2)
+        if h2d_ms else None,
+        "overlap": round(sum(t.overlap for t in recs) / K, 3),
+        "retained_bytes": int(st.retained_w + st.retained_kv),
+        "moved_bytes": int(st.moved_w + st.moved_kv),
+        "inflow_bytes": int(st.inflow_w + st.inflow_kv),
+        "reload_bytes": int(st.global_reload),
+        "reload_min_bytes": int(st.reload_min),
+        "kernels": kernels,
+        "roofline": {"bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "k_copy16", "call": "weights" if dk == 0 else "kv",
+                     "alg_bytes_per_launch": int(2 * db), "avg_launch_ms": round(dom_ms, 4)},
+    }
+    if not args.no_cpu_baseline:
+        if inplace:
+            fill_old()
+            torch.cuda.synchronize()
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_layers, aw, ak, hin_w, hin_k, table, pool)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, layers, aw, ak, hin_w, hin_k, table, pool):
+    """The oracle's plan execution (old shard + packed inflow -> new shard)
+    timed on the host for the first `layers` layers of the same workload."""
+    import copy as _copy
+
+    from oracle import model, repack
+
+    c = _copy.deepcopy(cfg)
+    c["layers"] = layers
+    pb = model.build(c)
+    _, o_size = pb.layout("old")
+    kv_old = pb.kv_arena_bytes("old", pool)
+    live = repack.live_blocks(table)
+    n_live = len(live)
+    w_in, k_in = repack.inflow_segments(pb, n_live)
+    w_in_b = sum(s[-1] for s in w_in)
+    k_in_b = sum(s[-1] for s in k_in)
+    old_w = aw[:o_size].cpu().numpy()
+    old_k = ak[:kv_old].cpu().numpy()
+    in_w = hin_w[:w_in_b].numpy().copy()
+    in_k = hin_k[:k_in_b].numpy().copy()
+    ret, _, _ = repack.self_bytes(pb, n_live)
+    t0 = time.perf_counter()
+    repack.apply_weights(pb, old_w, in_w)
+    repack.apply_kv(pb, old_k, in_k, table, pool)
+    dt = time.perf_counter() - t0
+    return {"value": round(2 * ret / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {layers} of {cfg['layers']} layers (weights + KV), "
+                      f"{2 * ret / 1e9:.2f} GB algorithmic, {dt:.2f} s, numpy single thread"}
+
+
+if __name__ == "__main__":
+    main()

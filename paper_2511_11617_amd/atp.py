@@ -13,7 +13,8 @@ import ctypes as C
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libatp.so")
+# ATP_LIB may name another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("ATP_LIB") or os.path.join(_HERE, "libatp.so")
 
 # ---- status codes and enums (atp.h) -----------------------------------------
 OK, EINVAL, ECAPACITY, EHIP, EALIGN, ESTATE = 0, -1, -2, -3, -4, -5

@@ -36,21 +36,24 @@ def _run(cmd):
     return r
 
 
-def build_atp(out_dir: str | None = None) -> str:
+def build_atp(out_dir: str | None = None, lib_path: str = LIB, defines=()) -> str:
+    """Compile libatp.so; `defines` (e.g. ["ATP_UNROLL=4"]) select a launch
+    shape other than the default (see csrc/desc.h)."""
     out_dir = out_dir or os.path.join(HERE, "_build")
     os.makedirs(out_dir, exist_ok=True)
+    dflags = ["-D" + d for d in defines]
     objs = []
     for src in ("plan.cpp", "capi.cpp"):
         obj = os.path.join(out_dir, src + ".o")
-        _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        _run(["g++", *HOST_FLAGS, *dflags, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     obj = os.path.join(out_dir, "exec.hip.o")
-    _run([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, "exec.hip"), "-o", obj])
+    _run([HIPCC, *DEVICE_FLAGS, *dflags, "-c", os.path.join(CSRC, "exec.hip"), "-o", obj])
     objs.append(obj)
-    tmp = LIB + ".tmp"
+    tmp = lib_path + ".tmp"
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 def build_synth() -> str:

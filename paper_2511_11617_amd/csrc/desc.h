@@ -31,9 +31,26 @@ enum : uint32_t {
                           // multiple of 16: the 16-byte vector kernel
 };
 
-// 16-byte chunks per tile of the vector kernel (256 threads x 8 chunks).
+// Launch shape of the vector kernel: 256 threads, ATP_UNROLL independent
+// 16-byte chunks per thread per tile; one workgroup per tile unless
+// ATP_PERSIST (grid-stride over tiles with a fixed grid).
+#ifndef ATP_UNROLL
+#define ATP_UNROLL 2
+#endif
+#ifndef ATP_PERSIST
+#define ATP_PERSIST 0
+#endif
+#ifndef ATP_NT_LOAD
+#define ATP_NT_LOAD 1
+#endif
+#ifndef ATP_NT_STORE
+#define ATP_NT_STORE 1
+#endif
+#ifndef ATP_XCD_MAP
+#define ATP_XCD_MAP 1
+#endif
 constexpr int kThreads = 256;
-constexpr int kUnroll = 8;
+constexpr int kUnroll = ATP_UNROLL;
 constexpr int64_t kTileChunks = kThreads * kUnroll;
 // bytes per tile of the 2-byte-granular (LDS funnel-shift) kernel
 constexpr int64_t kSegBytes = 8192;

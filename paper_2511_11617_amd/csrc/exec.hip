@@ -161,7 +161,9 @@ void check_extents(const CallPlan &c, bool kvcall, const Plan &P, uint64_t in_by
 
 void launch_copy(Exec &E, const Launch &L, const Desc *dev_desc, const int64_t *dev_prefix, char *b0, char *b1,
                  char *b2, const int32_t *live, hipStream_t s) {
-  uint64_t g = std::min<uint64_t>(std::max<uint64_t>(L.tiles_max, 1), uint64_t(E.grid_max));
+  // one workgroup per tile, or a fixed persistent grid
+  uint64_t cap = ATP_PERSIST ? uint64_t(E.grid_max) : (uint64_t(1) << 30);
+  uint64_t g = std::min<uint64_t>(std::max<uint64_t>(L.tiles_max, 1), cap);
   if (L.aligned)
     hipLaunchKernelGGL(k_copy16, dim3(unsigned(g)), dim3(kThreads), 0, s, dev_desc, dev_prefix, L.d0, L.d1, b0, b1,
                        b2, live);
@@ -401,6 +403,7 @@ int exec_sync(Plan &P, atp_timing *out) {
     return 0.0;
   };
   double h2d_ms = 0, rep_ms = 0;
+  hipEvent_t h2d_first = nullptr, h2d_last = nullptr;  // union span of both calls
   for (int which = 0; which < 2; ++which) {
     CallState &cs = which == 0 ? E.w : E.k;
     if (!cs.pending) continue;
@@ -422,7 +425,8 @@ int exec_sync(Plan &P, atp_timing *out) {
     double r = ms(cs.rep0, cs.rep1);
     (which == 0 ? t.repack_w_ms : t.repack_kv_ms) = r;
     rep_ms += r;
-    h2d_ms = std::max(h2d_ms, ms(cs.h2d0, cs.h2d1));
+    h2d_first = h2d_first ? h2d_first : cs.h2d0;
+    if (cs.h2d1) h2d_last = cs.h2d1;
     t.d2h_ms = std::max(t.d2h_ms, ms(cs.d2h0, cs.d2h1));
     for (const auto &L : cs.launches) {
       double m = ms(L.e0, L.e1);
@@ -434,6 +438,7 @@ int exec_sync(Plan &P, atp_timing *out) {
     t.d2h_bytes += cs.d2h_bytes;
     t.scatter_bytes += cs.scatter_bytes;
   }
+  h2d_ms = ms(h2d_first, h2d_last);
   t.h2d_ms = h2d_ms;
   t.wall_ms = E.wall_started
                   ? std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - E.wall0).count()

@@ -170,6 +170,36 @@ struct LineAddr {
   char *src, *dst;
 };
 
+// Streaming 16-byte accesses: nothing is read twice, so both sides carry
+// the non-temporal hint by default.
+__device__ __forceinline__ u32x4 load16(const u32x4 *p) {
+#if ATP_NT_LOAD
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
+__device__ __forceinline__ void store16(u32x4 *p, u32x4 v) {
+#if ATP_NT_STORE
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
+
+// First tile of this workgroup.  Workgroups are dealt round-robin to the
+// 8 XCDs; with ATP_XCD_MAP each XCD gets a contiguous run of tiles instead
+// of every 8th one.
+__device__ __forceinline__ int64_t tile_of_block() {
+#if ATP_XCD_MAP
+  const uint32_t G = gridDim.x, b = blockIdx.x, q = G >> 3, r = G & 7, xcd = b & 7, i = b >> 3;
+  return xcd < r ? int64_t(xcd) * (q + 1) + i : int64_t(r) * (q + 1) + int64_t(xcd - r) * q + i;
+#else
+  return blockIdx.x;
+#endif
+}
+
 __device__ __forceinline__ LineAddr line_addr(const Desc &x, uint32_t line, char *b0, char *b1, char *b2,
                                               const int32_t *__restrict__ live) {
   uint32_t orel = divq(line, x.magic_rows);
@@ -189,29 +219,50 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
                                                      int d0, int d1, char *b0, char *b1, char *b2,
                                                      const int32_t *__restrict__ live) {
   const int64_t T0 = prefix[d0], T1 = prefix[d1];
-  for (int64_t t = T0 + blockIdx.x; t < T1; t += gridDim.x) {
+  for (int64_t t = T0 + tile_of_block(); t < T1; t += gridDim.x) {
     const int d = find_desc(prefix, d0, d1, t);
     const Desc &x = descs[d];
     const uint32_t cpl = x.run >> 4;
     const uint64_t total = uint64_t(x.o_end - x.o_begin) * x.rows * cpl;
-    const uint64_t c0 = uint64_t(t - prefix[d]) * kTileChunks + threadIdx.x;
+    const uint64_t cbase = uint64_t(t - prefix[d]) * kTileChunks;
+    const uint64_t clast = (cbase + kTileChunks < total ? cbase + kTileChunks : total) - 1;
+    const uint32_t l0 = divq(uint32_t(cbase), x.magic_line);
     u32x4 v[kUnroll];
+    if (l0 == divq(uint32_t(clast), x.magic_line)) {
+      // the whole tile lies in one line: one address computation per tile
+      const LineAddr la = line_addr(x, l0, b0, b1, b2, live);
+      const uint32_t col0 = uint32_t(cbase) - l0 * cpl;
+      const uint32_t n = uint32_t(clast - cbase) + 1;
+      const u32x4 *s = reinterpret_cast<const u32x4 *>(la.src) + col0;
+      u32x4 *dd = reinterpret_cast<u32x4 *>(la.dst) + col0;
+#pragma unroll
+      for (int k = 0; k < kUnroll; ++k) {
+        const uint32_t i = threadIdx.x + k * kThreads;
+        if (i < n) v[k] = load16(s + i);
+      }
+#pragma unroll
+      for (int k = 0; k < kUnroll; ++k) {
+        const uint32_t i = threadIdx.x + k * kThreads;
+        if (i < n) store16(dd + i, v[k]);
+      }
+      continue;
+    }
     u32x4 *dp[kUnroll];
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
-      const uint64_t c = c0 + uint64_t(k) * kThreads;
+      const uint64_t c = cbase + threadIdx.x + uint64_t(k) * kThreads;
       dp[k] = nullptr;
-      if (c < total) {
+      if (c <= clast) {
         const uint32_t line = divq(uint32_t(c), x.magic_line);
         const uint32_t col = uint32_t(c) - line * cpl;
         LineAddr la = line_addr(x, line, b0, b1, b2, live);
-        v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(la.src) + col);
+        v[k] = load16(reinterpret_cast<const u32x4 *>(la.src) + col);
         dp[k] = reinterpret_cast<u32x4 *>(la.dst) + col;
       }
     }
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) __builtin_nontemporal_store(v[k], dp[k]);
+      if (dp[k]) store16(dp[k], v[k]);
   }
 }
 

@@ -68,12 +68,13 @@ def space_totals(shape: dict):
 class Built:
     """A Problem plus the arrays it points into."""
 
-    def __init__(self, problem, keep, tensors, n_live, pool):
+    def __init__(self, problem, keep, tensors, n_live, pool, old_ranges):
         self.problem = problem
         self.keep = keep
         self.tensors = tensors
         self.n_live = n_live
         self.pool = pool
+        self.old_ranges = old_ranges  # [space][old rank] -> (begin, end)
 
     def plan(self) -> atp.Plan:
         return atp.Plan(self.problem, keep=self.keep)
@@ -152,4 +153,4 @@ def build(shape: dict, n_live: int | None = None, pool: int | None = None, flags
                     pool, n_live)
         keep.append(kv)
         pb.kv = C.pointer(kv)
-    return Built(pb, keep, tl, n_live, pool)
+    return Built(pb, keep, tl, n_live, pool, [old[n] for n in names])

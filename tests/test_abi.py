@@ -1,0 +1,87 @@
+"""The C ABI: every function include/atp.h declares is exported by
+libatp.so, and planning rejects malformed problems with the documented
+codes (CPU; no GPU calls)."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2511_11617_amd import atp, problem
+from synth import configs
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "atp.h")
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(atp_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_header_functions_are_exported():
+    names = declared()
+    assert {"atp_plan", "atp_reshard_weights", "atp_reshard_kv", "atp_sync"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", atp.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (atp_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    for n in names:
+        assert hasattr(atp.lib, n)
+
+
+def _plan(c, **kw):
+    return problem.build(c, **kw).plan()
+
+
+def test_dead_self_rank_is_einval():
+    with pytest.raises(atp.AtpError) as e:
+        _plan(configs.get(1, self_old=1))
+    assert e.value.code == atp.EINVAL
+
+
+def test_new_tp_must_match_survivors():
+    with pytest.raises(atp.AtpError) as e:
+        _plan(configs.get(1, failed=[1, 2]))
+    assert e.value.code == atp.EINVAL
+
+
+def test_non_covering_explicit_ranges_are_einval():
+    c = configs.get(1, new_q_widths=None, new_ranges={"q": [(0, 2), (2, 3), (3, 3)]})
+    with pytest.raises(atp.AtpError) as e:
+        _plan(c)
+    assert e.value.code == atp.EINVAL
+    assert "cover" in str(e.value)
+
+
+def test_bad_gqa_reference_is_einval():
+    b = problem.build(configs.get(1))
+    b.problem.spaces[1].gqa_space = 1   # a space cannot follow itself
+    with pytest.raises(atp.AtpError) as e:
+        b.plan()
+    assert e.value.code == atp.EINVAL
+
+
+def test_in_place_staging_cap_too_small_is_ecapacity():
+    c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=256)
+    with pytest.raises(atp.AtpError) as e:
+        _plan(c, flags=atp.INPLACE, staging_cap=1 << 16)
+    assert e.value.code == atp.ECAPACITY
+
+
+def test_partition_helper():
+    assert atp.partition(1024, 3, atp.RULE_FLOOR) == [(0, 341), (341, 682), (682, 1024)]
+    assert atp.partition(688, 3, atp.RULE_CEIL_FIRST) == [(0, 230), (230, 459), (459, 688)]
+    with pytest.raises(atp.AtpError):
+        atp.partition(10, 0, atp.RULE_FLOOR)
+
+
+def test_planning_is_deterministic():
+    c = configs.scaled(5, layers=3, n_seq=2, seq_tokens=256)
+    a = _plan(c, flags=atp.INPLACE, staging_cap=2 << 30)
+    b = _plan(c, flags=atp.INPLACE, staging_cap=2 << 30)
+    sa, sb = a.stats(), b.stats()
+    for f, _ in atp.Stats._fields_:
+        assert getattr(sa, f) == getattr(sb, f), f
