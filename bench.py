@@ -56,6 +56,7 @@ def main():
     from paper_2511_11617_amd import atp, problem
     from synth import configs, fill, pagetable
     from synth.content import TAGS, Content
+    from synth.pinned import Pinned
 
     cfg = configs.get(args.workload)
     table, pool = pagetable.make_for(cfg)
@@ -87,10 +88,9 @@ def main():
     ak, nk = arena(st.old_kv_bytes, st.new_kv_bytes)
     stage_w = torch.empty(max(st.staging_w, 256), dtype=u8, device=dev)
     stage_k = torch.empty(max(st.staging_kv, 256), dtype=u8, device=dev)
-    hin_w = torch.empty(max(st.inflow_w, 1), dtype=u8, pin_memory=True)
-    hin_k = torch.empty(max(st.inflow_kv, 1), dtype=u8, pin_memory=True)
-    hout_w = torch.empty(max(st.outbound_w if inplace else 1, 1), dtype=u8, pin_memory=True)
-    hout_k = torch.empty(max(st.outbound_kv if inplace else 1, 1), dtype=u8, pin_memory=True)
+    hin_w, hin_k = Pinned(st.inflow_w), Pinned(st.inflow_kv)
+    hout_w = Pinned(st.outbound_w if inplace else 1)
+    hout_k = Pinned(st.outbound_kv if inplace else 1)
     table_d = torch.from_numpy(table).to(dev)
 
     # ---- synthetic content -----------------------------------------------------
@@ -115,18 +115,18 @@ def main():
         shards.append((TAGS[name], l, kind == atp.ROWS, rows, cols, unit, s.unit_begin, s.unit_end,
                        s.host_offset))
     fill.weights(tmp, content, shards)
-    hin_w.copy_(tmp[:hin_w.numel()])
+    hin_w.tensor.copy_(tmp[:hin_w.nbytes])
     segs = [(s.layer, s.which, s.unit_begin, s.unit_end, s.host_offset)
             for s in plan.segments(atp.SEG_INFLOW_KV)]
     fill.kv_packed(tmp, content, table, pool, segs, cfg["n_kv"], cfg["seq_tokens"], bt, hd, layout)
-    hin_k.copy_(tmp[:hin_k.numel()])
+    hin_k.tensor.copy_(tmp[:hin_k.nbytes])
     del tmp
     torch.cuda.synchronize()
     log(f"[bench] inputs generated in {time.time() - t0:.1f} s")
 
     compute = torch.cuda.current_stream()
     copy = torch.cuda.Stream()
-    ptr = lambda t: t.data_ptr() if t is not None else None
+    ptr = lambda t: None if t is None else (t.ptr if isinstance(t, Pinned) else t.data_ptr())
 
     def step():
         p = built.plan()
@@ -229,7 +229,8 @@ def main():
         if inplace:
             fill_old()
             torch.cuda.synchronize()
-        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_layers, aw, ak, hin_w, hin_k, table, pool)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_layers, aw, ak, hin_w.tensor, hin_k.tensor,
+                                           table, pool)
     print(json.dumps(out), flush=True)
 
 

@@ -289,6 +289,93 @@ def kv_live_mask(pb: Problem, table, pool: int, which: str) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
+# the definition evaluated word by word (full-size workloads, sampled)
+# ----------------------------------------------------------------------------
+def _groups(keys):
+    """(key, positions) for every distinct key, via one stable sort."""
+    order = np.argsort(keys, kind="stable")
+    ks = keys[order]
+    cuts = np.flatnonzero(np.diff(ks)) + 1
+    for part in np.split(order, cuts):
+        if part.size:
+            yield int(keys[part[0]]), part
+
+
+def expected_weight_words(pb: Problem, content, offsets):
+    """(words, valid) at even byte offsets of the NEW weight arena: the
+    16-bit word the definition puts there, and whether the offset lies in a
+    shard (not alignment padding).  Same definition as weight_arena(),
+    evaluated one position at a time."""
+    offs, _ = pb.layout("new")
+    offs = np.asarray(offs, dtype=np.int64)
+    q = np.asarray(offsets, dtype=np.int64)
+    ti = np.searchsorted(offs, q, side="right") - 1
+    words = np.zeros(q.shape, np.uint16)
+    valid = np.zeros(q.shape, bool)
+    for k, sel in _groups(ti):
+        t = pb.tensors[k]
+        a, b = pb.new_range(t.space)
+        r, c = t.shard_shape((a, b))
+        e = (q[sel] - offs[k]) // pb.eb
+        ok = e < r * c
+        sel, e = sel[ok], e[ok]
+        i, j = e // c, e % c
+        if t.kind == ROWS:
+            gi, gj = i + a * t.unit, j
+        else:
+            gi, gj = i, j + a * t.unit
+        words[sel] = content(t.tag, t.layer, (gi * t.cols + gj).astype(np.uint64))
+        valid[sel] = True
+    return words, valid
+
+
+def expected_packed_weight_words(pb: Problem, content, segments, offsets):
+    """Words at even byte offsets of a packed weight buffer (inflow or
+    outbound): segment (tensor, layer, which, kind, a, b, host_offset,
+    bytes) holds units [a, b) of the full tensor as a row-major rectangle."""
+    q = np.asarray(offsets, dtype=np.int64)
+    starts = np.array([s[6] for s in segments], dtype=np.int64)
+    si = np.searchsorted(starts, q, side="right") - 1
+    words = np.zeros(q.shape, np.uint16)
+    for k, sel in _groups(si):
+        ti, _, _, _, a, b, off, _ = segments[k]
+        t = pb.tensors[ti]
+        e = (q[sel] - off) // pb.eb
+        if t.kind == ROWS:
+            gi, gj = a * t.unit + e // t.cols, e % t.cols
+        else:
+            w = (b - a) * t.unit
+            gi, gj = e // w, a * t.unit + e % w
+        words[sel] = content(t.tag, t.layer, (gi * t.cols + gj).astype(np.uint64))
+    return words
+
+
+def expected_kv_words(pb: Problem, content, table, pool: int, offsets):
+    """(words, valid) at even byte offsets of the NEW KV arena; offsets in
+    free blocks are not valid.  Same definition as kv_arena()."""
+    c = pb.cfg
+    a, b = pb.kv_heads("new")
+    nh, bt, hd = b - a, pb.block_tokens, pb.head_dim
+    block = nh * bt * hd * pb.eb
+    q = np.asarray(offsets, dtype=np.int64)
+    g, rest = q // (pool * block), q % (pool * block)
+    p, inner = rest // block, (rest % block) // pb.eb
+    if pb.kv_layout == "head":
+        h, t, d = inner // (bt * hd), (inner // hd) % bt, inner % hd
+    else:
+        t, h, d = inner // (nh * hd), (inner // hd) % nh, inner % hd
+    seq, blk = _block_owner(table, pool)
+    s, lb = seq[p], blk[p]
+    valid = s >= 0
+    words = np.zeros(q.shape, np.uint16)
+    idx = ((s * c["seq_tokens"] + lb * bt + t) * pb.n_kv + (a + h)) * hd + d
+    for grp, sel in _groups(np.where(valid, g, -1)):
+        if grp >= 0:
+            words[sel] = content(10 + grp % 2, grp // 2, idx[sel].astype(np.uint64))
+    return words, valid
+
+
+# ----------------------------------------------------------------------------
 # packed-buffer segment lists (the packing order stated in the docstring)
 # ----------------------------------------------------------------------------
 def inflow_segments(pb: Problem, n_live: int):

@@ -247,12 +247,26 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
       }
       continue;
     }
+    // several lines per tile: resolve the line once per wavefront when its
+    // 64 chunks share one (short KV head runs), else per lane
     u32x4 *dp[kUnroll];
+    const uint32_t wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
+      const uint64_t g0 = cbase + uint64_t(k) * kThreads + wv * 64;
       const uint64_t c = cbase + threadIdx.x + uint64_t(k) * kThreads;
       dp[k] = nullptr;
-      if (c <= clast) {
+      if (g0 > clast) continue;
+      const uint64_t gl = g0 + 63 < clast ? g0 + 63 : clast;
+      const uint32_t lf = divq(uint32_t(g0), x.magic_line);
+      if (lf == divq(uint32_t(gl), x.magic_line)) {
+        const LineAddr la = line_addr(x, lf, b0, b1, b2, live);
+        const uint32_t col = uint32_t(c) - lf * cpl;
+        if (c <= clast) {
+          v[k] = load16(reinterpret_cast<const u32x4 *>(la.src) + col);
+          dp[k] = reinterpret_cast<u32x4 *>(la.dst) + col;
+        }
+      } else if (c <= clast) {
         const uint32_t line = divq(uint32_t(c), x.magic_line);
         const uint32_t col = uint32_t(c) - line * cpl;
         LineAddr la = line_addr(x, line, b0, b1, b2, live);

@@ -168,3 +168,26 @@ def test_outbound_pieces_are_dropped_parts():
     # old rank 2 sends FFN [459,516) to new rank 2 and keeps [344,459)
     pb2 = model.build(configs.get(1, self_old=2))
     assert repack._outbound_pieces(pb2, "ffn") == [(459, 516)]
+
+
+@settings(max_examples=30, deadline=None)
+@given(st.integers(0, 2 ** 31), st.booleans())
+def test_pointwise_definition_matches_materialised(seed, experts):
+    """The word-by-word evaluation used for full-size sampling agrees with
+    slicing the materialised full tensors, at every byte offset."""
+    c = tiny_cfg(random.Random(seed), experts)
+    pb = model.build(c)
+    content = Content(c["seed"], c["w_kind"], c["kv_kind"])
+    arena = repack.weight_arena(pb, content, "new")
+    mask = repack.weight_live_mask(pb, "new")
+    offs = np.arange(0, arena.size, 2)
+    words, valid = repack.expected_weight_words(pb, content, offs)
+    np.testing.assert_array_equal(valid, mask[offs])
+    np.testing.assert_array_equal(words[valid], arena.view(np.uint16)[valid])
+    table, pool = pagetable.make_for(c)
+    karena = repack.kv_arena(pb, content, table, pool, "new")
+    kmask = repack.kv_live_mask(pb, table, pool, "new")
+    koffs = np.arange(0, karena.size, 2)
+    kw, kv = repack.expected_kv_words(pb, content, table, pool, koffs)
+    np.testing.assert_array_equal(kv, kmask[koffs])
+    np.testing.assert_array_equal(kw[kv], karena.view(np.uint16)[kv])
