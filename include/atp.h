@@ -191,8 +191,11 @@ int atp_reshard_kv(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes,
 typedef struct {
   double plan_ms;      /* atp_plan host time                          */
   double wall_ms;      /* first reshard call -> atp_sync return        */
-  double repack_w_ms;  /* compute-stream span of the weight repack     */
-  double repack_kv_ms; /* compute-stream span of the KV repack         */
+  double repack_w_ms;  /* weight repack kernels, summed launch times    */
+  double repack_kv_ms; /* KV repack kernels, summed launch times        */
+  double repack_span_ms; /* first -> last repack launch of each call,
+                            summed; in place it includes the waits for
+                            outbound reads                               */
   double h2d_ms;       /* copy-stream span of the inflow copies        */
   double d2h_ms;       /* span of the outbound copies (in place)       */
   double scatter_ms;   /* summed landing-ring scatter kernel time      */

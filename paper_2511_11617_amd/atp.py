@@ -70,7 +70,7 @@ class Problem(C.Structure):
 
 class Timing(C.Structure):
     _fields_ = [("plan_ms", C.c_double), ("wall_ms", C.c_double), ("repack_w_ms", C.c_double),
-                ("repack_kv_ms", C.c_double), ("h2d_ms", C.c_double), ("d2h_ms", C.c_double),
+                ("repack_kv_ms", C.c_double), ("repack_span_ms", C.c_double), ("h2d_ms", C.c_double), ("d2h_ms", C.c_double),
                 ("scatter_ms", C.c_double), ("overlap", C.c_double), ("repack_bytes", C.c_uint64),
                 ("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("scatter_bytes", C.c_uint64),
                 ("n_launches", C.c_int32), ("reserved", C.c_int32)]
