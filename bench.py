@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", type=int, default=2,
                     help="1..5; 2 = dense 40L h5120 TP 4->3 (the headline workload)")
+    ap.add_argument("--plan", choices=["cm", "greedy", "full"], default="cm",
+                    help="planner: CMM (Alg. 1) or the Greedy / Full Reload baselines of Sec. V")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the CPU oracle over the whole workload for at least this long")
@@ -81,7 +83,8 @@ def main():
     table, pool = pagetable.make_for(cfg)
     n_live = int(len(np.unique(table[table >= 0])))
     inplace = bool(cfg["inplace"])
-    flags = atp.INPLACE if inplace else 0
+    flags = (atp.INPLACE if inplace else 0) | {"cm": 0, "greedy": atp.PLAN_GREEDY,
+                                               "full": atp.PLAN_FULL}[args.plan]
     cap = cfg["staging_cap"] or 0
     built = problem.build(cfg, n_live=n_live, pool=pool, flags=flags, staging_cap=cap)
     plan = built.plan()
@@ -194,7 +197,7 @@ def main():
     alg = 2 * (st.moved_w + st.moved_kv)
     rep_ms = sum(t.repack_w_ms + t.repack_kv_ms for t in recs) / K
     span_ms = sum(t.repack_span_ms for t in recs) / K
-    value = alg / (rep_ms * 1e-3) / 1e9
+    value = alg / (rep_ms * 1e-3) / 1e9 if rep_ms > 0 else 0.0  # Full Reload keeps nothing
     wall_ms = elapsed / K * 1e3
     h2d_ms = sum(t.h2d_ms for t in recs) / K
     # dominant kernel: the repack launch moving the most bytes
@@ -203,13 +206,13 @@ def main():
         for kind, level, b, ms in L:
             if kind in (0, 1):
                 per.setdefault((kind, level, b), []).append(ms)
-    (dk, dl, db), dms = max(per.items(), key=lambda kv: kv[0][2])
+    (dk, dl, db), dms = max(per.items(), key=lambda kv: kv[0][2]) if per else ((0, 0, 0), [0.0])
     traffic = None
     counted = COUNTED_TRAFFIC.get(cfg["name"])
-    if counted and kernel_src_hash() == COUNTED_TRAFFIC["src"]:
+    if counted and args.plan == "cm" and kernel_src_hash() == COUNTED_TRAFFIC["src"]:
         traffic = counted.get("weights" if dk == 0 else "kv")
     dom_ms = sum(dms) / len(dms)
-    dom_gbps = 2 * db / (dom_ms * 1e-3) / 1e9
+    dom_gbps = 2 * db / (dom_ms * 1e-3) / 1e9 if dom_ms > 0 else 0.0
     kernels = [{"call": "weights" if k == 0 else "kv",
                 "level": l, "alg_bytes": 2 * b, "avg_ms": round(sum(v) / len(v), 4),
                 "GBps": round(2 * b / (sum(v) / len(v) * 1e-3) / 1e9, 1)}
@@ -232,7 +235,8 @@ def main():
                    "tp": f"{cfg['old_tp']}->{cfg['new_tp']}", "failed": cfg["failed"],
                    "self_old_rank": self_old, "self_new_rank": st.self_new_rank,
                    "kv_sequences": cfg["n_seq"], "seq_tokens": cfg["seq_tokens"],
-                   "in_place": inplace, "elem": "bf16" if cfg["elem_bytes"] == 2 else "?"},
+                   "in_place": inplace, "elem": "fp16" if cfg["w_kind"] == 1 else "bf16",
+                   "planner": args.plan},
         "hbm_frac": round(value / HBM_PEAK_GBPS, 4),
         "repack_ms": round(rep_ms, 4),
         "repack_span_ms": round(span_ms, 4),

@@ -165,13 +165,19 @@ class Task:
         return (self.kind, self.begin, self.end, self.src, self.dst, self.host)
 
 
-def cmm(old_ranges, failed, targets, owner):
+def cmm(old_ranges, failed, targets, owner, variant="cm"):
     """The CMM loop of Alg. 1 for one space.
 
     old_ranges[i] is old rank i's range (dead ranks included); `targets` is
     the list of target ranges; owner[j] is the old rank hosting target j.
     Tasks come out target by target; within a target, transfers in source
     order (host first, then ascending rank), then reloads in range order.
+
+    variant (the planner baselines of Sec. V, Table 2):
+      "cm"      Alg. 1
+      "greedy"  keep what the host already holds; every gap is reloaded,
+                no cross-device transfer
+      "full"    no reuse: the whole target is reloaded
     """
     dead = set(failed)
     N = len(old_ranges)
@@ -180,7 +186,7 @@ def cmm(old_ranges, failed, targets, owner):
         tar = [tgt] if tgt[0] < tgt[1] else []
         order = [owner[j]] + [i for i in range(N) if i != owner[j]]
         for i in order:
-            if i in dead:
+            if i in dead or variant == "full" or (variant == "greedy" and i != owner[j]):
                 continue
             inter = iv_intersect(tar, old_ranges[i])
             if inter:

@@ -173,7 +173,7 @@ def _old_ranges(cfg, name, total, N, q_old):
     return cmm.even_ranges(total, N)
 
 
-def build(cfg: dict, assign: str = "inorder") -> Problem:
+def build(cfg: dict, assign: str = "inorder", variant: str = "cm") -> Problem:
     """The oracle's view of workload `cfg` and its per-space CMM plans."""
     N, M = cfg["old_tp"], cfg["new_tp"]
     failed = list(cfg["failed"])
@@ -207,5 +207,5 @@ def build(cfg: dict, assign: str = "inorder") -> Problem:
                  block_tokens=cfg["block_tokens"], head_dim=cfg["head_dim"],
                  kv_layout=cfg.get("kv_layout", "head"), n_kv=cfg["n_kv"])
     for name in sp:
-        pb.plans[name] = cmm.cmm(old[name], failed, new[name], owner)
+        pb.plans[name] = cmm.cmm(old[name], failed, new[name], owner, variant)
     return pb

@@ -42,10 +42,10 @@ def say(msg):
     sys.stdout.flush()
 
 
-def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name=""):
+def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm"):
     say(f"[gpu case] {name} cfg={c.get('name', '?')} layers={c['layers']} flags={flags} "
         f"old_tp={c['old_tp']} new_tp={c['new_tp']} failed={c['failed']} self_old={c['self_old']}")
-    pb = model.build(c, assign=assign)
+    pb = model.build(c, assign=assign, variant=variant)
     content = CachedContent(Content(c["seed"], c["w_kind"], c["kv_kind"]))
     table, pool = pagetable.make_for(c)
     n_live = int(len(repack.live_blocks(table)))

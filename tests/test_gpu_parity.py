@@ -69,3 +69,10 @@ def test_large_shapes_one_layer(n):
 def test_cfg5_shape_in_place_two_layers():
     c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
     run_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"], name="cfg5-2layers-inplace")
+
+
+@pytest.mark.parametrize("variant,flag", [("greedy", atp.PLAN_GREEDY), ("full", atp.PLAN_FULL)])
+@pytest.mark.parametrize("inplace", [False, True])
+def test_planner_baselines(variant, flag, inplace):
+    flags = flag | (atp.INPLACE if inplace else 0)
+    run_case(configs.get(1), flags=flags, variant=variant, name=f"cfg1-{variant}")

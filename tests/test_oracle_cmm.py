@@ -261,3 +261,31 @@ def test_cfg1_hand_values():
                 p2p += (x.end - x.begin) * ub
     assert rel == int(g["global_reload_per_layer"][0])
     assert p2p == int(g["global_p2p_per_layer"][0])
+
+
+def test_planner_baselines_fig3():
+    """Sec. V planner baselines on the Fig. 3 example: Greedy keeps only
+    what each host holds and reloads every gap (no cross-device transfer);
+    Full Reload reuses nothing.  Table 2's ordering CM < Greedy < Full
+    holds in reloaded rows."""
+    old = [(0, 256), (256, 512), (512, 768), (768, 1024)]
+    targets = cmm.floor_targets(1024, 3)
+    owner = [0, 2, 3]
+    r = {v: cmm.reload_units(cmm.cmm(old, [1], targets, owner, v)) for v in ("cm", "greedy", "full")}
+    assert r == {"cm": 256, "greedy": 85 + 171 + 86, "full": 1024}
+    g = cmm.cmm(old, [1], targets, owner, "greedy")
+    assert all(x.kind in (cmm.KEEP, cmm.RELOAD) for x in g)
+
+
+def test_planner_baselines_random():
+    for old, failed, targets in _tiny_cases(300, seed=5):
+        owner = cmm.assign_inorder(len(old), failed, len(targets))
+        cm = cmm.reload_units(cmm.cmm(old, failed, targets, owner))
+        gr = cmm.cmm(old, failed, targets, owner, "greedy")
+        fu = cmm.cmm(old, failed, targets, owner, "full")
+        # Greedy reloads exactly what the host does not hold
+        want_gr = sum((v - u) - max(0, min(old[owner[j]][1], v) - max(old[owner[j]][0], u))
+                      for j, (u, v) in enumerate(targets))
+        assert cmm.reload_units(gr) == want_gr
+        assert cmm.reload_units(fu) == sum(v - u for u, v in targets)
+        assert cm <= cmm.reload_units(gr) <= cmm.reload_units(fu)
