@@ -301,8 +301,9 @@ typedef struct {
   int32_t op, level;
   int32_t src_buf, dst_buf;
   int32_t flags;
-  int32_t after_d2h; /* H2D: the first after_d2h D2H copies of this list
-                        (issued in list order) must have finished      */
+  int32_t after_d2h; /* H2D, SCATTER: the first after_d2h D2H copies of
+                        this list (issued in list order) must have
+                        finished                                        */
   uint64_t src_off, dst_off, src_pitch, dst_pitch, src_stride, dst_stride;
   int64_t item_begin, item_end;
   uint64_t run, rows;

@@ -101,10 +101,30 @@ class Launch(C.Structure):
     _fields_ = [("kind", C.c_int32), ("level", C.c_int32), ("bytes", C.c_uint64), ("ms", C.c_double)]
 
 
+def hip_runtimes():
+    """Distinct libamdhip64 files mapped into this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({line.split()[-1] for line in f if "libamdhip64" in line})
+    except OSError:
+        return []
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2511_11617_amd.build`")
+    # torch ships its own HIP runtime under the same soname as the system's.
+    # Mapping torch's first makes this library bind to it; the other order
+    # leaves two runtimes in the process, and this library's calls would then
+    # act on streams and memory that the other runtime created.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = C.CDLL(LIB_PATH)
+    runtimes = hip_runtimes()
+    if len(runtimes) > 1:
+        raise ImportError("two HIP runtimes are mapped in this process: " + ", ".join(runtimes))
     P = C.c_void_p
     lib.atp_plan.argtypes = [C.POINTER(Problem), C.POINTER(P)]
     lib.atp_plan_free.argtypes = [P]

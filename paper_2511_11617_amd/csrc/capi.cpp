@@ -213,20 +213,13 @@ int atp_plan_copies(const atp_plan_t *plan, int32_t which, atp_copy *out, int32_
   std::vector<atp_copy> v;
   // outbound reads first, in the order the executor issues them (by the
   // level that needs them); each must finish before that level
-  std::vector<int> pos(c.outbound.size(), -1);
   if (P.inplace) {
     std::vector<int> need(c.outbound.size(), INT32_MAX);
     for (const atp::Launch &L : c.levels)
       for (int o : L.wait_outbound) need[o] = std::min(need[o], L.level);
-    std::vector<int> ord;
-    for (size_t o = 0; o < c.outbound.size(); ++o)
-      if (c.outbound[o].dev_buf != atp::BUF_STAGE) ord.push_back(int(o));
-    std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return need[a] < need[b]; });
-    for (size_t k = 0; k < ord.size(); ++k) {
-      int o = ord[k];
-      pos[o] = int(k);
-      v.push_back(host_copy(c.outbound[o], ATP_COPY_D2H, need[o] == INT32_MAX ? -1 : need[o], true));
-    }
+    for (int o : c.out_order)
+      if (c.outbound[o].dev_buf != atp::BUF_STAGE)
+        v.push_back(host_copy(c.outbound[o], ATP_COPY_D2H, need[o] == INT32_MAX ? -1 : need[o], true));
   }
   for (const atp::Launch &L : c.levels)
     for (int d = L.d0; d < L.d1; ++d) v.push_back(dev_copy(c.fams[d], ATP_COPY_REPACK, L.level));
@@ -235,13 +228,17 @@ int atp_plan_copies(const atp_plan_t *plan, int32_t which, atp_copy *out, int32_
       if (h.dev_buf == atp::BUF_STAGE) v.push_back(host_copy(h, ATP_COPY_D2H, 1, true));
   for (const atp::HostCopy &h : c.directs) {
     atp_copy x = host_copy(h, ATP_COPY_H2D, h.gate_level, false);
-    for (int o : h.gate_out) x.after_d2h = std::max(x.after_d2h, pos[o] + 1);
+    x.after_d2h = h.gate_pos;
     v.push_back(x);
   }
   for (const atp::Chunk &ch : c.chunks) {
     for (const atp::HostCopy &h : ch.copies) v.push_back(host_copy(h, ATP_COPY_H2D_RING, -1, false));
     for (const atp::Launch &L : ch.scatters)
-      for (int d = L.d0; d < L.d1; ++d) v.push_back(dev_copy(c.fams[d], ATP_COPY_SCATTER, -1));
+      for (int d = L.d0; d < L.d1; ++d) {
+        atp_copy x = dev_copy(c.fams[d], ATP_COPY_SCATTER, -1);
+        x.after_d2h = ch.gate_pos;
+        v.push_back(x);
+      }
   }
   return copy_out(v, out, cap, n);
 }

@@ -9,6 +9,8 @@
 
 #include <algorithm>
 #include <chrono>
+#include <map>
+#include <mutex>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -38,6 +40,7 @@ struct CallState {
   int32_t *err_host = nullptr;  // pinned error word
   hipEvent_t start = nullptr;  // marks the caller's work queued before the call
   hipEvent_t tail_compute = nullptr, tail_copy = nullptr, tail_d2h = nullptr;
+  hipEvent_t tail_late_copy = nullptr, tail_late_comp = nullptr;
   hipEvent_t rep0 = nullptr, rep1 = nullptr, h2d0 = nullptr, h2d1 = nullptr, d2h0 = nullptr, d2h1 = nullptr;
   struct LaunchRec {
     int kind, level;
@@ -48,10 +51,23 @@ struct CallState {
   uint64_t h2d_bytes = 0, d2h_bytes = 0, scatter_bytes = 0, repack_bytes = 0;
 };
 
+// Process-wide recycling of HIP objects per device.  Each plan owns what it
+// takes until it is freed; creating events, streams and pinned buffers for
+// every plan would otherwise cost tens of milliseconds per reshard.
+struct DevicePool {
+  std::vector<hipEvent_t> sync_ev, time_ev;
+  std::vector<hipStream_t> streams;
+  std::vector<std::pair<void *, size_t>> pinned;
+};
+std::mutex g_pool_mu;
+std::map<int, DevicePool> g_pools;
+
 struct Exec {
   int device = -1;
   int grid_max = 2048;
-  hipStream_t d2h = nullptr;
+  hipStream_t d2h = nullptr;    // outbound reads (in place)
+  hipStream_t copy2 = nullptr;  // in-place weight landings that wait for levels / outbound reads
+  hipStream_t comp2 = nullptr;  // in-place weight levels and scatters
   std::vector<hipEvent_t> sync_pool, time_pool;
   size_t sync_used = 0, time_used = 0;
   CallState w, k;
@@ -62,28 +78,79 @@ struct Exec {
 
   hipEvent_t ev_sync() {
     if (sync_used == sync_pool.size()) {
-      hipEvent_t e;
-      HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+      hipEvent_t e = nullptr;
+      {
+        std::lock_guard<std::mutex> g(g_pool_mu);
+        auto &v = g_pools[device].sync_ev;
+        if (!v.empty()) {
+          e = v.back();
+          v.pop_back();
+        }
+      }
+      if (!e) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
       sync_pool.push_back(e);
     }
     return sync_pool[sync_used++];
   }
   hipEvent_t ev_time() {
     if (time_used == time_pool.size()) {
-      hipEvent_t e;
-      HIPCHK(hipEventCreate(&e));
+      hipEvent_t e = nullptr;
+      {
+        std::lock_guard<std::mutex> g(g_pool_mu);
+        auto &v = g_pools[device].time_ev;
+        if (!v.empty()) {
+          e = v.back();
+          v.pop_back();
+        }
+      }
+      if (!e) HIPCHK(hipEventCreate(&e));
       time_pool.push_back(e);
     }
     return time_pool[time_used++];
   }
-  ~Exec() {
-    for (hipEvent_t e : sync_pool) (void)hipEventDestroy(e);
-    for (hipEvent_t e : time_pool) (void)hipEventDestroy(e);
-    for (CallState *c : {&w, &k}) {
-      if (c->desc_host) (void)hipHostFree(c->desc_host);
-      if (c->err_host) (void)hipHostFree(c->err_host);
+  hipStream_t stream() {
+    {
+      std::lock_guard<std::mutex> g(g_pool_mu);
+      auto &v = g_pools[device].streams;
+      if (!v.empty()) {
+        hipStream_t s = v.back();
+        v.pop_back();
+        return s;
+      }
     }
-    if (d2h) (void)hipStreamDestroy(d2h);
+    hipStream_t s;
+    HIPCHK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));  // default priority
+    return s;
+  }
+  void *pinned(size_t bytes, size_t *cap) {
+    {
+      std::lock_guard<std::mutex> g(g_pool_mu);
+      auto &v = g_pools[device].pinned;
+      for (size_t i = 0; i < v.size(); ++i)
+        if (v[i].second >= bytes) {
+          void *p = v[i].first;
+          *cap = v[i].second;
+          v.erase(v.begin() + long(i));
+          return p;
+        }
+    }
+    void *p = nullptr;
+    HIPCHK(hipHostMalloc(&p, bytes, hipHostMallocDefault));
+    *cap = bytes;
+    return p;
+  }
+  ~Exec() {
+    // hand everything back for the next plan on this device
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    DevicePool &pl = g_pools[device];
+    pl.sync_ev.insert(pl.sync_ev.end(), sync_pool.begin(), sync_pool.end());
+    pl.time_ev.insert(pl.time_ev.end(), time_pool.begin(), time_pool.end());
+    for (CallState *c : {&w, &k}) {
+      if (c->desc_host) pl.pinned.push_back({c->desc_host, c->desc_cap * sizeof(Desc)});
+      if (c->err_host) pl.pinned.push_back({c->err_host, 256});
+    }
+    for (hipStream_t st : {d2h, copy2, comp2})
+      if (st) pl.streams.push_back(st);
   }
 };
 
@@ -99,13 +166,12 @@ Exec &exec_of(Plan &P) {
   return *static_cast<Exec *>(P.exec);
 }
 
-void build_descs(const CallPlan &c, CallState &cs) {
+void build_descs(Exec &E, const CallPlan &c, CallState &cs) {
   size_t n = c.fams.size();
-  if (cs.desc_host && cs.desc_cap >= n) return;
-  if (cs.desc_host) HIPCHK(hipHostFree(cs.desc_host));
-  HIPCHK(hipHostMalloc(reinterpret_cast<void **>(&cs.desc_host), std::max<size_t>(n, 1) * sizeof(Desc),
-                       hipHostMallocDefault));
-  cs.desc_cap = std::max<size_t>(n, 1);
+  if (cs.desc_host) return;  // the descriptors of a plan never change
+  size_t cap = 0;
+  cs.desc_host = static_cast<Desc *>(E.pinned(std::max<size_t>(n, 1) * sizeof(Desc), &cap));
+  cs.desc_cap = cap / sizeof(Desc);
   for (size_t i = 0; i < n; ++i) {
     const Fam &f = c.fams[i];
     Desc d{};
@@ -224,11 +290,14 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     E.wall_started = true;
     E.wall0 = std::chrono::steady_clock::now();
   }
-  if (!cs.err_host) HIPCHK(hipHostMalloc(reinterpret_cast<void **>(&cs.err_host), 256, hipHostMallocDefault));
+  if (!cs.err_host) {
+    size_t cap = 0;
+    cs.err_host = static_cast<int32_t *>(E.pinned(256, &cap));
+  }
   *cs.err_host = 0;
   cs.launches.clear();
   cs.h2d_bytes = cs.d2h_bytes = cs.scatter_bytes = cs.repack_bytes = 0;
-  build_descs(c, cs);
+  build_descs(E, c, cs);
 
   char *b_in = static_cast<char *>(arena), *b_out = static_cast<char *>(new_arena),
        *b_st = static_cast<char *>(staging);
@@ -251,6 +320,15 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   }
   cs.start = start;
   HIPCHK(hipStreamWaitEvent(copy, start, 0));
+
+  // landings that depend on nothing go first, so that the link is busy at once
+  cs.h2d0 = E.ev_time();
+  HIPCHK(hipEventRecord(cs.h2d0, copy));
+  for (const HostCopy &h : c.directs)
+    if (h.gate_pos == 0 && h.gate_level < 0) {
+      HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
+      cs.h2d_bytes += h.bytes;
+    }
 
   // ---- upload descriptors, prepare ----------------------------------------------
   if (!c.fams.empty())
@@ -275,20 +353,15 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   HIPCHK(hipGetLastError());
 
   // ---- outbound (in place): read before overwrite ---------------------------------
-  std::vector<hipEvent_t> out_ev(c.outbound.size(), nullptr);
+  // issued in the plan's order (by the first level that overwrites them);
+  // pos_ev[k] fires when the first k + 1 of them have finished
+  std::vector<hipEvent_t> out_ev(c.outbound.size(), nullptr), pos_ev;
   if (do_out && !kvcall) {
-    if (!E.d2h) HIPCHK(hipStreamCreateWithFlags(&E.d2h, hipStreamNonBlocking));
+    if (!E.d2h) E.d2h = E.stream();
     HIPCHK(hipStreamWaitEvent(E.d2h, start, 0));
     cs.d2h0 = E.ev_time();
     HIPCHK(hipEventRecord(cs.d2h0, E.d2h));
-    // issue in the order later writers need them
-    std::vector<int> ord(c.outbound.size());
-    for (size_t i = 0; i < ord.size(); ++i) ord[i] = int(i);
-    std::vector<int> need(c.outbound.size(), INT32_MAX);
-    for (const Launch &L : c.levels)
-      for (int o : L.wait_outbound) need[o] = std::min(need[o], L.level);
-    std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return need[a] < need[b]; });
-    for (int o : ord) {
+    for (int o : c.out_order) {
       const HostCopy &h = c.outbound[o];
       if (h.rows <= 1)
         HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_in + h.dev_off, h.bytes, hipMemcpyDeviceToHost, E.d2h));
@@ -297,38 +370,56 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
                                 hipMemcpyDeviceToHost, E.d2h));
       out_ev[o] = E.ev_sync();
       HIPCHK(hipEventRecord(out_ev[o], E.d2h));
+      pos_ev.push_back(out_ev[o]);
       cs.d2h_bytes += h.bytes;
     }
     cs.d2h1 = E.ev_time();
     HIPCHK(hipEventRecord(cs.d2h1, E.d2h));
   }
 
+  // In place, the weight levels wait for outbound reads; that work and
+  // everything after it (ring landings, scatters, gated landings) runs on
+  // two library streams so that it does not hold up the caller's streams,
+  // and with them the other call's work.
+  const bool split = do_out && !kvcall;
+  hipStream_t late_copy = copy, late_comp = compute;
+  if (split) {
+    if (!E.copy2) E.copy2 = E.stream();
+    if (!E.comp2) E.comp2 = E.stream();
+    late_copy = E.copy2;
+    late_comp = E.comp2;
+    hipEvent_t prepared = E.ev_sync();
+    HIPCHK(hipEventRecord(prepared, compute));
+    HIPCHK(hipStreamWaitEvent(late_comp, prepared, 0));
+    HIPCHK(hipStreamWaitEvent(late_copy, start, 0));
+  }
+
   // ---- repack levels ---------------------------------------------------------------
   std::vector<hipEvent_t> level_end(std::max(c.n_levels, 1), nullptr);
   cs.rep0 = E.ev_time();
-  HIPCHK(hipEventRecord(cs.rep0, compute));
+  HIPCHK(hipEventRecord(cs.rep0, late_comp));
   for (size_t i = 0; i < c.levels.size(); ++i) {
     const Launch &L = c.levels[i];
     for (int o : L.wait_outbound)
-      if (out_ev[o]) HIPCHK(hipStreamWaitEvent(compute, out_ev[o], 0));
+      if (out_ev[o]) HIPCHK(hipStreamWaitEvent(late_comp, out_ev[o], 0));
     CallState::LaunchRec r{kvcall ? 1 : 0, L.level, L.bytes, E.ev_time(), E.ev_time()};
-    HIPCHK(hipEventRecord(r.e0, compute));
-    launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, compute);
-    HIPCHK(hipEventRecord(r.e1, compute));
+    HIPCHK(hipEventRecord(r.e0, late_comp));
+    launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
+    HIPCHK(hipEventRecord(r.e1, late_comp));
     cs.launches.push_back(r);
     cs.repack_bytes += 2 * L.bytes;
     bool last_of_level = i + 1 == c.levels.size() || c.levels[i + 1].level != L.level;
     if (last_of_level) {
       level_end[L.level] = E.ev_sync();
-      HIPCHK(hipEventRecord(level_end[L.level], compute));
+      HIPCHK(hipEventRecord(level_end[L.level], late_comp));
     }
   }
   cs.rep1 = E.ev_time();
-  HIPCHK(hipEventRecord(cs.rep1, compute));
+  HIPCHK(hipEventRecord(cs.rep1, late_comp));  // also: prepare and every level are done
 
   // KV outbound gathered into staging at level 0: copy it out after that level
   if (do_out && kvcall) {
-    if (!E.d2h) HIPCHK(hipStreamCreateWithFlags(&E.d2h, hipStreamNonBlocking));
+    if (!E.d2h) E.d2h = E.stream();
     if (level_end[0]) HIPCHK(hipStreamWaitEvent(E.d2h, level_end[0], 0));
     cs.d2h0 = E.ev_time();
     HIPCHK(hipEventRecord(cs.d2h0, E.d2h));
@@ -342,47 +433,49 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   }
 
   // ---- inflow ------------------------------------------------------------------------
-  cs.h2d0 = E.ev_time();
-  HIPCHK(hipEventRecord(cs.h2d0, copy));
-  auto direct = [&](const HostCopy &h) {
-    if (h.gate_level >= 0 && level_end[h.gate_level]) HIPCHK(hipStreamWaitEvent(copy, level_end[h.gate_level], 0));
-    for (int o : h.gate_out)
-      if (out_ev[o]) HIPCHK(hipStreamWaitEvent(copy, out_ev[o], 0));
-    HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
+  auto gate_out = [&](hipStream_t s, int gate_pos) {
+    if (gate_pos > 0 && gate_pos <= int(pos_ev.size())) HIPCHK(hipStreamWaitEvent(s, pos_ev[gate_pos - 1], 0));
+  };
+  auto direct = [&](const HostCopy &h, hipStream_t s) {
+    if (h.gate_level >= 0 && level_end[h.gate_level]) HIPCHK(hipStreamWaitEvent(s, level_end[h.gate_level], 0));
+    gate_out(s, h.gate_pos);
+    HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, s));
     cs.h2d_bytes += h.bytes;
   };
+  // (ungated landings were issued first) those waiting for levels only
   for (const HostCopy &h : c.directs)
-    if (h.gate_level < 0 && h.gate_out.empty()) direct(h);
-  // ring: H2D into a slot on `copy`, scatter from it on `compute`
-  if (!c.chunks.empty() && do_out && !kvcall)
-    for (hipEvent_t e : out_ev)
-      if (e) HIPCHK(hipStreamWaitEvent(compute, e, 0));
+    if (h.gate_pos == 0 && h.gate_level >= 0) direct(h, late_copy);
+  // ring: H2D into a slot, scatter from it after every level (and after the
+  // outbound reads the chunk overwrites)
   std::vector<hipEvent_t> slot_free(c.chunks.size(), nullptr);
   for (size_t i = 0; i < c.chunks.size(); ++i) {
     const Chunk &ch = c.chunks[i];
-    if (i >= size_t(c.n_slots) && slot_free[i - c.n_slots]) HIPCHK(hipStreamWaitEvent(copy, slot_free[i - c.n_slots], 0));
+    hipStream_t cs_copy = late_copy, cs_comp = late_comp;  // scatters after every level
+    if (i >= size_t(c.n_slots) && slot_free[i - c.n_slots])
+      HIPCHK(hipStreamWaitEvent(cs_copy, slot_free[i - c.n_slots], 0));
     for (const HostCopy &h : ch.copies) {
-      HIPCHK(hipMemcpyAsync(b_st + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
+      HIPCHK(hipMemcpyAsync(b_st + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, cs_copy));
       cs.h2d_bytes += h.bytes;
     }
     hipEvent_t landed = E.ev_sync();
-    HIPCHK(hipEventRecord(landed, copy));
-    HIPCHK(hipStreamWaitEvent(compute, landed, 0));
+    HIPCHK(hipEventRecord(landed, cs_copy));
+    HIPCHK(hipStreamWaitEvent(cs_comp, landed, 0));
+    gate_out(cs_comp, ch.gate_pos);
     for (const Launch &L : ch.scatters) {
       CallState::LaunchRec r{2, -1, L.bytes, E.ev_time(), E.ev_time()};
-      HIPCHK(hipEventRecord(r.e0, compute));
-      launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, compute);
-      HIPCHK(hipEventRecord(r.e1, compute));
+      HIPCHK(hipEventRecord(r.e0, cs_comp));
+      launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, cs_comp);
+      HIPCHK(hipEventRecord(r.e1, cs_comp));
       cs.launches.push_back(r);
       cs.scatter_bytes += L.bytes;
     }
     slot_free[i] = E.ev_sync();
-    HIPCHK(hipEventRecord(slot_free[i], compute));
+    HIPCHK(hipEventRecord(slot_free[i], cs_comp));
   }
   for (const HostCopy &h : c.directs)
-    if (!(h.gate_level < 0 && h.gate_out.empty())) direct(h);
+    if (h.gate_pos > 0) direct(h, late_copy);
   cs.h2d1 = E.ev_time();
-  HIPCHK(hipEventRecord(cs.h2d1, copy));
+  HIPCHK(hipEventRecord(cs.h2d1, late_copy));
 
   // ---- tails ----------------------------------------------------------------------
   HIPCHK(hipMemcpyAsync(cs.err_host, dev_err, sizeof(int32_t), hipMemcpyDeviceToHost, compute));
@@ -390,10 +483,18 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   HIPCHK(hipEventRecord(cs.tail_compute, compute));
   cs.tail_copy = E.ev_sync();
   HIPCHK(hipEventRecord(cs.tail_copy, copy));
-  cs.tail_d2h = nullptr;
+  cs.tail_d2h = cs.tail_late_copy = cs.tail_late_comp = nullptr;
   if (do_out) {
     cs.tail_d2h = E.ev_sync();
     HIPCHK(hipEventRecord(cs.tail_d2h, E.d2h));
+  }
+  if (split) {
+    // the late streams are not joined back into the caller's streams (that
+    // would hold up the other call's work); atp_sync waits for them
+    cs.tail_late_copy = E.ev_sync();
+    HIPCHK(hipEventRecord(cs.tail_late_copy, late_copy));
+    cs.tail_late_comp = E.ev_sync();
+    HIPCHK(hipEventRecord(cs.tail_late_comp, late_comp));
   }
   cs.pending = true;
 }
@@ -416,7 +517,7 @@ int exec_sync(Plan &P, atp_timing *out) {
   for (int which = 0; which < 2; ++which) {
     CallState &cs = which == 0 ? E.w : E.k;
     if (!cs.pending) continue;
-    for (hipEvent_t e : {cs.tail_compute, cs.tail_copy, cs.tail_d2h}) {
+    for (hipEvent_t e : {cs.tail_compute, cs.tail_copy, cs.tail_d2h, cs.tail_late_copy, cs.tail_late_comp}) {
       if (!e) continue;
       hipError_t err = hipEventSynchronize(e);
       if (err != hipSuccess && rc == ATP_OK) {
@@ -472,7 +573,7 @@ void exec_free(Plan &P) {
     // drain anything still queued before the pinned buffers go away
     for (CallState *c : {&E->w, &E->k})
       if (c->pending)
-        for (hipEvent_t e : {c->tail_compute, c->tail_copy, c->tail_d2h})
+        for (hipEvent_t e : {c->tail_compute, c->tail_copy, c->tail_d2h, c->tail_late_copy, c->tail_late_comp})
           if (e) (void)hipEventSynchronize(e);
     delete E;
     P.exec = nullptr;

@@ -616,6 +616,7 @@ bool is_identity(const Fam &f) {
 }
 
 constexpr uint64_t kSplitLine = 64 * 1024;
+constexpr uint64_t kDirectMin = 32ull << 20;  // smallest inflow gap landed directly
 constexpr size_t kMaxPieces = 1u << 20;
 
 struct Node {
@@ -982,6 +983,13 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
         if (needed_by[o] == l) c.levels[before].wait_outbound.push_back(int(o));
     }
   }
+  // outbound issue order: by the first level that overwrites it
+  std::vector<int> pos(outbound.size(), 0);
+  c.out_order.resize(outbound.size());
+  std::iota(c.out_order.begin(), c.out_order.end(), 0);
+  std::stable_sort(c.out_order.begin(), c.out_order.end(),
+                   [&](int a, int b) { return needed_by[a] < needed_by[b]; });
+  for (size_t k = 0; k < c.out_order.size(); ++k) pos[c.out_order[k]] = int(k);
   // outbound host copies
   for (size_t o = 0; o < outbound.size(); ++o) {
     const Pending &pd = outbound[o];
@@ -1024,10 +1032,19 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
       oidx.build();
     }
   }
-  std::vector<const Pending *> ring;
+  // outbound copies a landing on `d` must wait for: the first k in issue order
+  auto out_gate = [&](Span d) {
+    int k = 0;
+    if (P.inplace && !kvcall) oidx.query(d, [&](int o) { k = std::max(k, pos[o] + 1); });
+    return k;
+  };
+  std::vector<std::pair<int, const Pending *>> ring;  // (outbound gate, piece)
   uint64_t ring_total = 0, max_item = 0;
   for (const Pending &pd : inflow) {
-    if (pd.contiguous) {
+    // Only large contiguous gaps land directly: every copy command costs the
+    // copy engine a fraction of a millisecond, so small gaps travel in large
+    // sequential chunks through the landing ring and a scatter places them.
+    if (pd.contiguous && pd.fam.bytes() >= kDirectMin) {
       HostCopy h;
       h.host_off = pd.host_off;
       h.dev_off = pd.fam.dst_off;
@@ -1039,19 +1056,26 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
           int l = nodes[a].kind == Node::NORMAL ? nodes[a].level : 0;
           h.gate_level = std::max(h.gate_level, l);
         });
-        if (!kvcall) oidx.query(d, [&](int o) { h.gate_out.push_back(o); });
+        h.gate_pos = out_gate(d);
       }
       c.directs.push_back(h);
     } else {
-      ring.push_back(&pd);
-      ring_total += pd.fam.bytes();
-      max_item = std::max<uint64_t>(max_item, pd.fam.rows * pd.fam.run);
+      const Fam &f = pd.fam;
+      int g = (f.flags & DF_DST_IND) ? 0 : out_gate(dst_span(f, f.o_begin, f.o_end));
+      ring.push_back({g, &pd});
+      ring_total += f.bytes();
+      max_item = std::max<uint64_t>(max_item, f.rows * f.run);
     }
   }
-  // in place, direct landings go in gate order so early ones are not
-  // blocked behind late ones
-  std::stable_sort(c.directs.begin(), c.directs.end(),
-                   [](const HostCopy &a, const HostCopy &b) { return a.gate_level < b.gate_level; });
+  // in place, landings go in gate order so that early ones are not blocked
+  // behind late ones
+  std::stable_sort(c.directs.begin(), c.directs.end(), [](const HostCopy &a, const HostCopy &b) {
+    return std::make_pair(a.gate_pos, a.gate_level) < std::make_pair(b.gate_pos, b.gate_level);
+  });
+  std::stable_sort(ring.begin(), ring.end(),
+                   [](const std::pair<int, const Pending *> &a, const std::pair<int, const Pending *> &b) {
+                     return a.first < b.first;
+                   });
 
   uint64_t slot = 0;
   if (!ring.empty()) {
@@ -1081,16 +1105,20 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
       ch = Chunk();
       fill = 0;
     };
-    for (const Pending *pd : ring) {
+    for (const auto &gp : ring) {
+      const Pending *pd = gp.second;
       const Fam &f = pd->fam;
       uint64_t item = f.rows * f.run;
       int64_t k = f.o_begin;
+      // gated pieces start a chunk of their own kind
+      if (!pieces.empty() && (ch.gate_pos > 0) != (gp.first > 0)) flush();
       while (k < f.o_end) {
         int64_t room = int64_t((slot - fill) / item);
         if (room <= 0) {
           flush();
           continue;
         }
+        ch.gate_pos = std::max(ch.gate_pos, gp.first);
         int64_t k1 = std::min<int64_t>(f.o_end, k + room);
         // host copy of items [k, k1) into the slot at `fill`
         uint64_t hoff = pd->host_off + uint64_t(k - f.o_begin) * item;

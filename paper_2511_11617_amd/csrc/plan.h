@@ -72,7 +72,8 @@ struct HostCopy {
   uint64_t bytes = 0;
   int dev_buf = BUF_OUT;      // BUF_OUT for direct landing, BUF_STAGE ring
   int gate_level = -1;        // in place: level whose reads must finish
-  std::vector<int> gate_out;  // outbound copies that must finish
+  int gate_pos = 0;           // in place: the first gate_pos outbound copies
+                              // (in issue order) must finish first
   // strided device side (outbound): rows x run at dev pitch
   uint64_t rows = 1, run = 0, dev_pitch = 0;
 };
@@ -80,6 +81,7 @@ struct HostCopy {
 // Landing-ring chunk: H2D into a slot, then scatter launch(es) from it.
 struct Chunk {
   int slot = 0;
+  int gate_pos = 0;               // outbound copies its scatter must wait for
   std::vector<HostCopy> copies;   // into the slot
   std::vector<Launch> scatters;   // aligned and/or 2-byte-granular
 };
@@ -91,6 +93,7 @@ struct CallPlan {
   std::vector<HostCopy> directs;
   std::vector<Chunk> chunks;
   std::vector<HostCopy> outbound;
+  std::vector<int> out_order;   // outbound issue order (by the level needing it)
   std::vector<atp_segment> seg_in, seg_out;
   int n_levels = 0;
   uint64_t retained = 0, moved = 0, staged = 0;

@@ -30,6 +30,9 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB_PATH):
             raise ImportError(f"{_LIB_PATH} missing: run `python -m paper_2511_11617_amd.build`")
+        # torch's own HIP runtime must be mapped before this library, or the
+        # process would hold two HIP runtimes (they share a soname)
+        import torch  # noqa: F401
         L = C.CDLL(_LIB_PATH)
         L.synth_fill.argtypes = [C.c_void_p, C.POINTER(Region), C.c_int, C.c_void_p]
         L.synth_fill_kv.argtypes = [C.c_void_p, C.c_uint64, C.c_void_p, C.c_void_p, C.c_void_p,

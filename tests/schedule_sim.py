@@ -190,11 +190,17 @@ def replay(cps, bufs: dict, live: np.ndarray):
                 written[x.dst_buf].append((dst, dst + x.run))
         state["levels_done"] = L + 1
         land_ready()
+    # landing ring, after every level: a scatter first waits for the outbound
+    # reads it is gated on (outbound reads still happen as late as allowed)
+    for x in cps:
+        if x.op in (H2D_RING, SCATTER):
+            if x.op == SCATTER:
+                d2h_until(lambda y: state["d2h_done"] < x.after_d2h)
+            src, dst = _lines(x, live)
+            move(x, src, dst)
+            if x.op == SCATTER and x.dst_buf in written:
+                written[x.dst_buf].append((dst, dst + x.run))
     d2h_until(lambda x: True)
     land_ready()
     if pending:
         raise Hazard("inflow landing whose gates never open")
-    for x in cps:
-        if x.op in (H2D_RING, SCATTER):
-            src, dst = _lines(x, live)
-            move(x, src, dst)

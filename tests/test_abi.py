@@ -32,6 +32,20 @@ def test_header_functions_are_exported():
         assert hasattr(atp.lib, n)
 
 
+def test_one_hip_runtime_whatever_the_import_order():
+    # torch bundles a HIP runtime with the system's soname: loading the
+    # library before torch must not leave a second runtime in the process
+    code = ("import paper_2511_11617_amd.atp as atp\n"
+            "from synth import gpu, pinned\n"
+            "gpu.lib(); pinned._lib()\n"
+            "import torch\n"
+            "rt = atp.hip_runtimes()\n"
+            "assert len(rt) == 1 and 'torch' in rt[0], rt\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run(["python", "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+
+
 def _plan(c, **kw):
     return problem.build(c, **kw).plan()
 
