@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--plan", choices=["cm", "greedy", "full"], default="cm",
                     help="planner: CMM (Alg. 1) or the Greedy / Full Reload baselines of Sec. V")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--load", action="store_true",
+                    help="also time the range-read reload source (atp_load_weights) on a checkpoint "
+                         "written for this workload")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the CPU oracle over the whole workload for at least this long")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
@@ -259,6 +262,8 @@ def main():
                      "kernel": "k_copy16", "call": "weights" if dk == 0 else "kv",
                      "alg_bytes_per_launch": int(2 * db), "avg_launch_ms": round(dom_ms, 4)},
     }
+    if args.load:
+        out["load"] = load_leg(args.steps, cfg, plan, st, tl, hin_w, Pinned)
     if not args.no_cpu_baseline:
         if inplace:
             fill_old()
@@ -266,6 +271,66 @@ def main():
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, aw, ak, hin_w.tensor, hin_k.tensor,
                                            table, pool)
     print(json.dumps(out), flush=True)
+
+
+def load_leg(steps, cfg, plan, st, tl, hin_w, Pinned):
+    """Range-read reload source (atp_load_weights).  The checkpoint has the
+    headers of every full weight tensor; as data it holds the intervals this
+    plan reads, taken from the synthetic inflow, and holes elsewhere (the full
+    model would not fit the scratch disk).  The reads hit a warm page cache."""
+    import shutil
+    import tempfile
+
+    from paper_2511_11617_amd import atp
+    from synth import checkpoint
+
+    if st.inflow_w == 0:
+        return {"skipped": "this plan reads no weights"}
+    tens = [(n, l, rows, cols) for (n, l, k, sp, rows, cols, u) in tl]
+    names = [checkpoint.name(n, l) for (n, l, *_) in tl]
+    src = hin_w.tensor.numpy()
+    regions = []
+    for s in plan.segments(atp.SEG_INFLOW_W):
+        n, l, kind, sp, rows, cols, unit = tl[s.tensor]
+        a, b = s.unit_begin * unit, s.unit_end * unit
+        w = src[s.host_offset:s.host_offset + s.bytes].view(np.uint16)
+        if kind == atp.ROWS:
+            regions.append((n, l, cols, a, b, 0, cols, w.reshape(b - a, cols)))
+        else:
+            regions.append((n, l, cols, 0, rows, a, b, w.reshape(rows, b - a)))
+    # strided tensors are written whole over the rows they span: allow 3x
+    # the read bytes; a memory-backed directory first (no writeback throttle)
+    need = 3 * st.inflow_w + (2 << 30)
+    where = [x for x in ("/dev/shm", tempfile.gettempdir())
+             if os.path.isdir(x) and os.access(x, os.W_OK) and shutil.disk_usage(x).free >= need]
+    if not where:
+        return {"skipped": f"no scratch directory with {need / 1e9:.1f} GB free"}
+    d = tempfile.mkdtemp(prefix="atp_ckpt_", dir=where[0])
+    try:
+        path = os.path.join(d, "model.safetensors")
+        t0 = time.time()
+        total = checkpoint.write_stream(path, tens, regions, "fp16" if cfg["w_kind"] == 1 else "bf16")
+        write_s = time.time() - t0
+        log(f"[bench] checkpoint written in {write_s:.1f} s ({total / 1e9:.1f} GB logical)")
+        files = atp.StFiles([path])
+        buf = Pinned(st.inflow_w, fill=0xA5)
+        ms = []
+        for i in range(steps + 1):  # the first pass is a warm-up
+            ls = plan.load_weights(files, names, buf.ptr, st.inflow_w)
+            if i:
+                ms.append(ls.read_ms)
+        if not np.array_equal(buf.tensor.numpy(), src):
+            raise RuntimeError("range reads returned other bytes than the checkpoint holds")
+        files.close()
+        buf.close()
+    finally:
+        shutil.rmtree(d, ignore_errors=True)
+    read_ms = sum(ms) / len(ms)
+    return {"source": f"safetensors range reads, file in {where[0]} (page cache)", "bytes": int(st.inflow_w),
+            "tensor_bytes": int(ls.tensor_bytes), "read_fraction": round(st.inflow_w / ls.tensor_bytes, 4),
+            "reads": int(ls.reads), "threads": int(ls.threads), "read_ms": round(read_ms, 3),
+            "GBps": round(st.inflow_w / (read_ms * 1e-3) / 1e9, 2), "file_bytes": int(total),
+            "write_s": round(write_s, 2)}
 
 
 def h2d_probe(torch, bufs, max_bytes, stream, chunk=64 << 20):

@@ -314,6 +314,58 @@ int atp_plan_copies(const atp_plan_t *plan, int32_t which, atp_copy *out, int32_
  * CEIL_FIRST). */
 int atp_partition(int64_t total, int32_t parts, int32_t rule, atp_range *out);
 
+/* ---- range-read reload source (Sec. IV: the loader reads safetensors by
+ * offsets, fetching only the byte intervals it needs) ---------------------- */
+typedef struct atp_st_obj atp_st_t;
+
+/* Open `n_paths` safetensors files and parse their headers: an 8-byte
+ * little-endian header length, a JSON object of name -> {dtype, shape,
+ * data_offsets}, then the data.  Every tensor is checked: known dtype,
+ * offsets inside the data, size = product(shape) x dtype size, names unique
+ * across the files.  Any violation gives ATP_EINVAL and *out stays unset.
+ * The files stay open until atp_st_close. */
+int atp_st_open(const char *const *paths, int32_t n_paths, atp_st_t **out);
+void atp_st_close(atp_st_t *st);
+
+typedef struct {
+  int32_t file;        /* index into the paths given to atp_st_open      */
+  int32_t elem_bytes;  /* bytes per element of the dtype                 */
+  int32_t ndim;        /* rank of the shape (shape[] holds the first 8)  */
+  int64_t shape[8];
+  uint64_t offset, bytes; /* absolute byte range of the data in the file */
+} atp_st_tensor;
+/* Look a tensor up by name; ATP_EINVAL if no file holds it. */
+int atp_st_find(const atp_st_t *st, const char *name, atp_st_tensor *out);
+
+typedef struct {
+  double read_ms;         /* wall time of the range reads                 */
+  uint64_t bytes;         /* bytes read (= the plan's weight inflow)       */
+  uint64_t reads;         /* pread calls issued                            */
+  uint64_t tensor_bytes;  /* data bytes of the named tensors: what a full
+                             reload of them would read                     */
+  int32_t threads;        /* reader threads used                           */
+} atp_load_stats;
+
+/* Fill the plan's packed weight inflow buffer (atp_plan_segments,
+ * ATP_SEG_INFLOW_W) from the files, reading only the needed intervals:
+ *   names        one tensor name per problem tensor (problem order); the
+ *                named tensor must be 2-D [rows, cols] with the problem
+ *                tensor's rows, cols and elem_bytes (experts stacked as the
+ *                problem states them)
+ *   inflow_host  host buffer of exactly stats.inflow_w bytes (pinned for the
+ *                reshard that follows); written in the plan's packing order:
+ *                ATP_ROWS units [a, b) are rows [a*unit, b*unit), one
+ *                interval; ATP_COLS units are columns, one interval per row,
+ *                packed row after row
+ *   n_threads    reader threads, <= 0 for min(16, hardware threads)
+ *   stats        may be NULL
+ * Synchronous; safe to call while a reshard of another plan runs.  A missing
+ * name, a shape or element-size mismatch, a wrong buffer size or a failed
+ * read gives ATP_EINVAL (the buffer is then partly written). */
+int atp_load_weights(const atp_plan_t *plan, const atp_st_t *st, const char *const *names,
+                     int32_t n_names, void *inflow_host, uint64_t inflow_bytes,
+                     int32_t n_threads, atp_load_stats *stats);
+
 const char *atp_last_error(void);
 
 #ifdef __cplusplus

@@ -33,7 +33,7 @@ EXPORTS = [
     "atp_plan", "atp_plan_free", "atp_reshard_weights", "atp_reshard_kv", "atp_sync",
     "atp_plan_stats", "atp_plan_tasks", "atp_plan_ranges", "atp_plan_owner",
     "atp_plan_layout", "atp_plan_segments", "atp_plan_launches", "atp_partition",
-    "atp_last_error",
+    "atp_last_error", "atp_st_open", "atp_st_close", "atp_st_find", "atp_load_weights",
 ]
 
 
@@ -101,6 +101,16 @@ class Launch(C.Structure):
     _fields_ = [("kind", C.c_int32), ("level", C.c_int32), ("bytes", C.c_uint64), ("ms", C.c_double)]
 
 
+class StTensor(C.Structure):
+    _fields_ = [("file", C.c_int32), ("elem_bytes", C.c_int32), ("ndim", C.c_int32),
+                ("shape", C.c_int64 * 8), ("offset", C.c_uint64), ("bytes", C.c_uint64)]
+
+
+class LoadStats(C.Structure):
+    _fields_ = [("read_ms", C.c_double), ("bytes", C.c_uint64), ("reads", C.c_uint64),
+                ("tensor_bytes", C.c_uint64), ("threads", C.c_int32)]
+
+
 def hip_runtimes():
     """Distinct libamdhip64 files mapped into this process."""
     try:
@@ -143,9 +153,16 @@ def _load():
     lib.atp_plan_segments.argtypes = [P, C.c_int32, C.POINTER(Segment), C.c_int32, C.POINTER(C.c_int32)]
     lib.atp_plan_launches.argtypes = [P, C.POINTER(Launch), C.c_int32, C.POINTER(C.c_int32)]
     lib.atp_partition.argtypes = [C.c_int64, C.c_int32, C.c_int32, C.POINTER(Range)]
+    lib.atp_st_open.argtypes = [C.POINTER(C.c_char_p), C.c_int32, C.POINTER(P)]
+    lib.atp_st_close.argtypes = [P]
+    lib.atp_st_close.restype = None
+    lib.atp_st_find.argtypes = [P, C.c_char_p, C.POINTER(StTensor)]
+    lib.atp_load_weights.argtypes = [P, P, C.POINTER(C.c_char_p), C.c_int32, P, C.c_uint64, C.c_int32,
+                                     C.POINTER(LoadStats)]
     lib.atp_last_error.restype = C.c_char_p
     for f in EXPORTS:
-        getattr(lib, f).restype = getattr(lib, f).restype if f in ("atp_plan_free", "atp_last_error") else C.c_int
+        if f not in ("atp_plan_free", "atp_last_error", "atp_st_close"):
+            getattr(lib, f).restype = C.c_int
     return lib
 
 
@@ -241,3 +258,37 @@ class Plan:
         t = Timing()
         _check(lib.atp_sync(self.h, C.byref(t)))
         return t
+
+    def load_weights(self, files: "StFiles", names, inflow, inflow_bytes, threads=0) -> LoadStats:
+        """Fill the weight inflow buffer at address `inflow` from `files`."""
+        arr = (C.c_char_p * len(names))(*[n.encode() for n in names])
+        st = LoadStats()
+        _check(lib.atp_load_weights(self.h, files.h, arr, len(names), inflow, inflow_bytes, threads,
+                                    C.byref(st)))
+        return st
+
+
+class StFiles:
+    """Opened safetensors files (atp_st_open)."""
+
+    def __init__(self, paths):
+        arr = (C.c_char_p * len(paths))(*[os.fsencode(p) for p in paths])
+        h = C.c_void_p()
+        _check(lib.atp_st_open(arr, len(paths), C.byref(h)))
+        self.h = h
+
+    def find(self, name: str):
+        t = StTensor()
+        _check(lib.atp_st_find(self.h, name.encode(), C.byref(t)))
+        return t.file, t.elem_bytes, tuple(t.shape[:t.ndim]), t.offset, t.bytes
+
+    def close(self):
+        if self.h:
+            lib.atp_st_close(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

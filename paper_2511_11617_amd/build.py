@@ -24,7 +24,7 @@ ARCH = "gfx950"
 DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                 "-Wall", "-Wno-unused-function"]
-HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wextra", "-Wno-unused-parameter",
+HOST_FLAGS = ["-O2", "-fPIC", "-pthread", "-std=c++17", "-Wall", "-Wextra", "-Wno-unused-parameter",
               "-I/opt/rocm/include", "-D__HIP_PLATFORM_AMD__"]
 
 
@@ -43,7 +43,7 @@ def build_atp(out_dir: str | None = None, lib_path: str = LIB, defines=()) -> st
     os.makedirs(out_dir, exist_ok=True)
     dflags = ["-D" + d for d in defines]
     objs = []
-    for src in ("plan.cpp", "capi.cpp"):
+    for src in ("plan.cpp", "loader.cpp", "capi.cpp"):
         obj = os.path.join(out_dir, src + ".o")
         _run(["g++", *HOST_FLAGS, *dflags, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
@@ -51,7 +51,7 @@ def build_atp(out_dir: str | None = None, lib_path: str = LIB, defines=()) -> st
     _run([HIPCC, *DEVICE_FLAGS, *dflags, "-c", os.path.join(CSRC, "exec.hip"), "-o", obj])
     objs.append(obj)
     tmp = lib_path + ".tmp"
-    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp])
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-pthread", *objs, "-o", tmp])
     os.replace(tmp, lib_path)
     return lib_path
 

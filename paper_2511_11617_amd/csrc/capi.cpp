@@ -8,10 +8,15 @@
 
 #include "../../include/atp.h"
 #include "exec.h"
+#include "loader.h"
 #include "plan.h"
 
 struct atp_plan_obj {
   atp::Plan *p;
+};
+
+struct atp_st_obj {
+  atp::StFiles *f;
 };
 
 namespace {
@@ -249,6 +254,48 @@ int atp_partition(int64_t total, int32_t parts, int32_t rule, atp_range *out) {
     std::vector<atp::Rng> r;
     atp::partition(total, parts, rule, r);
     for (int i = 0; i < parts; ++i) out[i] = {r[i].b, r[i].e};
+    return ATP_OK;
+  });
+}
+
+int atp_st_open(const char *const *paths, int32_t n_paths, atp_st_t **out) {
+  return guard([&]() -> int {
+    if (!out) return fail(ATP_EINVAL, "out is NULL");
+    atp::StFiles *f = atp::st_open(paths, n_paths);
+    *out = new atp_st_obj{f};
+    return ATP_OK;
+  });
+}
+
+void atp_st_close(atp_st_t *st) {
+  if (!st) return;
+  delete st->f;
+  delete st;
+}
+
+int atp_st_find(const atp_st_t *st, const char *name, atp_st_tensor *out) {
+  return guard([&]() -> int {
+    if (!st || !name || !out) return fail(ATP_EINVAL, "st, name or out is NULL");
+    auto it = st->f->map.find(name);
+    if (it == st->f->map.end()) return fail(ATP_EINVAL, std::string("no tensor named '") + name + "'");
+    const atp::StTensor &t = it->second;
+    atp_st_tensor o{};
+    o.file = t.file;
+    o.elem_bytes = t.elem_bytes;
+    o.ndim = int32_t(t.shape.size());
+    for (size_t i = 0; i < t.shape.size() && i < 8; ++i) o.shape[i] = int64_t(t.shape[i]);
+    o.offset = t.begin;
+    o.bytes = t.end - t.begin;
+    *out = o;
+    return ATP_OK;
+  });
+}
+
+int atp_load_weights(const atp_plan_t *plan, const atp_st_t *st, const char *const *names, int32_t n_names,
+                     void *inflow_host, uint64_t inflow_bytes, int32_t n_threads, atp_load_stats *stats) {
+  return guard([&]() -> int {
+    if (!plan || !st) return fail(ATP_EINVAL, "plan or st is NULL");
+    atp::load_weights(*plan->p, *st->f, names, n_names, inflow_host, inflow_bytes, n_threads, stats);
     return ATP_OK;
   });
 }

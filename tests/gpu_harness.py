@@ -7,6 +7,7 @@ inflow buffer and the block table.
 """
 from __future__ import annotations
 
+import os
 import sys
 
 import numpy as np
@@ -15,7 +16,7 @@ import torch
 from oracle import model, repack
 from paper_2511_11617_amd import atp, problem
 from synth import pagetable
-from synth.content import Content
+from synth.content import KIND_FP16, Content
 
 POISON = 0xA5
 
@@ -42,7 +43,12 @@ def say(msg):
     sys.stdout.flush()
 
 
-def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm"):
+def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
+             ckpt_dir=None):
+    """Reshard one workload on the GPU and compare with the oracle.  With
+    `ckpt_dir`, the weight inflow is read from a safetensors checkpoint
+    written there by the library's range-read loader instead of being copied
+    from the oracle's packed inflow."""
     say(f"[gpu case] {name} cfg={c.get('name', '?')} layers={c['layers']} flags={flags} "
         f"old_tp={c['old_tp']} new_tp={c['new_tp']} failed={c['failed']} self_old={c['self_old']}")
     pb = model.build(c, assign=assign, variant=variant)
@@ -89,6 +95,17 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
     stage_w = torch.full((max(st.staging_w, 256),), 0x5A, dtype=u8, device=dev)
     stage_k = torch.full((max(st.staging_kv, 256),), 0x5A, dtype=u8, device=dev)
     hin_w, hin_k = pinned(in_w), pinned(in_k)
+    if ckpt_dir is not None and in_w.size:
+        from synth import checkpoint
+        tl = problem.tensor_list(c)
+        path = os.path.join(str(ckpt_dir), "model.safetensors")
+        checkpoint.write_package(path, Content(c["seed"], c["w_kind"], c["kv_kind"]),
+                                 [(n, l, r, cc) for (n, l, k, sp, r, cc, u) in tl],
+                                 "fp16" if c["w_kind"] == KIND_FP16 else "bf16")
+        hin_w.fill_(0xA5)  # the loader must write every byte
+        files = atp.StFiles([path])
+        plan.load_weights(files, [checkpoint.name(n, l) for (n, l, *_) in tl], hin_w.data_ptr(), in_w.size)
+        files.close()
     hout_w = torch.full((max(st.outbound_w, 1),), 0x3C, dtype=u8, pin_memory=True)
     hout_k = torch.full((max(st.outbound_kv, 1),), 0x3C, dtype=u8, pin_memory=True)
     table_d = torch.from_numpy(table).to(dev)
