@@ -59,6 +59,10 @@ def parse():
     ap.add_argument("--plan", choices=["cm", "greedy", "full"], default="cm",
                     help="planner: CMM (Alg. 1) or the Greedy / Full Reload baselines of Sec. V")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kv-budget", type=float, default=None,
+                    help="KV budget as a fraction of the new layout's live KV demand: sessions (seeded "
+                         "recency) are evicted least recently used first (atp_kv_evict_lru); out of "
+                         "place the kept blocks land in a compact arena (ATP_KV_COMPACT)")
     ap.add_argument("--load", action="store_true",
                     help="also time the range-read reload source (atp_load_weights) on a checkpoint "
                          "written for this workload")
@@ -89,6 +93,22 @@ def main():
     flags = (atp.INPLACE if inplace else 0) | {"cm": 0, "greedy": atp.PLAN_GREEDY,
                                                "full": atp.PLAN_FULL}[args.plan]
     cap = cfg["staging_cap"] or 0
+    full_table, evict = table, None
+    if args.kv_budget is not None:
+        pre = problem.build(cfg, n_live=n_live, pool=pool, flags=flags, staging_cap=cap).plan().stats()
+        bb = pre.new_kv_bytes // pool
+        last_use = np.random.default_rng(cfg["seed"] + 1).permutation(table.shape[0])
+        budget = int(args.kv_budget * n_live * bb)
+        keep, table, est = atp.kv_evict_lru(full_table, last_use, pool, bb, budget)
+        n_live = int(est.live_after)
+        if not inplace:
+            flags |= atp.KV_COMPACT
+        evict = {"budget_bytes": budget, "block_bytes": int(bb), "kept_sessions": int(est.kept_sessions),
+                 "evicted_sessions": int(est.evicted_sessions), "live_before": int(est.live_before),
+                 "live_after": int(est.live_after), "demand_before": int(est.demand_before),
+                 "demand_after": int(est.demand_after), "compact": bool(flags & atp.KV_COMPACT)}
+        log(f"[bench] KV budget {args.kv_budget}: kept {est.kept_sessions} of {table.shape[0]} sessions, "
+            f"{est.live_after} of {est.live_before} blocks")
     built = problem.build(cfg, n_live=n_live, pool=pool, flags=flags, staging_cap=cap)
     plan = built.plan()
     st = plan.stats()
@@ -129,7 +149,7 @@ def main():
             a, b = old_r[sp][self_old]
             shards.append((TAGS[name], l, kind == atp.ROWS, rows, cols, unit, a, b, plan.layout(i)[0]))
         fill.weights(aw, content, shards)
-        fill.kv_arena(ak, content, table, pool, cfg["layers"], old_r[1][self_old], cfg["n_kv"],
+        fill.kv_arena(ak, content, full_table, pool, cfg["layers"], old_r[1][self_old], cfg["n_kv"],
                       cfg["seq_tokens"], bt, hd, layout)
 
     fill_old()
@@ -239,7 +259,7 @@ def main():
                    "self_old_rank": self_old, "self_new_rank": st.self_new_rank,
                    "kv_sequences": cfg["n_seq"], "seq_tokens": cfg["seq_tokens"],
                    "in_place": inplace, "elem": "fp16" if cfg["w_kind"] == 1 else "bf16",
-                   "planner": args.plan},
+                   "planner": args.plan, "kv_budget": args.kv_budget},
         "hbm_frac": round(value / HBM_PEAK_GBPS, 4),
         "repack_ms": round(rep_ms, 4),
         "repack_span_ms": round(span_ms, 4),
@@ -262,9 +282,11 @@ def main():
                      "kernel": "k_copy16", "call": "weights" if dk == 0 else "kv",
                      "alg_bytes_per_launch": int(2 * db), "avg_launch_ms": round(dom_ms, 4)},
     }
+    if evict is not None:
+        out["kv_evict"] = evict
     if args.load:
         out["load"] = load_leg(args.steps, cfg, plan, st, tl, hin_w, Pinned)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and evict is None:  # the oracle's leg runs the by-id layout
         if inplace:
             fill_old()
             torch.cuda.synchronize()

@@ -104,7 +104,10 @@ typedef struct {
  * (HEAD_MAJOR) or [layer][K,V][num_blocks][block_tokens][heads][head_dim]
  * (TOKEN_MAJOR), heads = the rank's KV-head range of `space`.  Physical
  * block ids are unchanged by the reshard; live_blocks is the number of
- * distinct ids the block table references. */
+ * distinct ids the block table references.  With ATP_KV_COMPACT the new
+ * arena has live_blocks blocks per (layer, K|V) plane instead of num_blocks,
+ * and live block p lands at its rank among the live ids (ascending): the
+ * caller renumbers its table the same way (atp_kv_evict_lru does). */
 enum { ATP_KV_HEAD_MAJOR = 0, ATP_KV_TOKEN_MAJOR = 1 };
 
 typedef struct {
@@ -124,7 +127,10 @@ enum {
   ATP_ASSIGN_MAXRETAIN = 1, /* survivor permutation keeping most bytes   */
   ATP_INPLACE = 1 << 4,     /* new layout overwrites the old arena       */
   ATP_PLAN_GREEDY = 1 << 8, /* Sec. V baseline: keep local, reload gaps  */
-  ATP_PLAN_FULL = 1 << 9    /* Sec. V baseline: reload every byte        */
+  ATP_PLAN_FULL = 1 << 9,   /* Sec. V baseline: reload every byte        */
+  ATP_KV_COMPACT = 1 << 10  /* new KV arena holds only the live blocks,  */
+                            /* block p at its rank among the live ids    */
+                            /* (out of place only; see atp_kv_evict_lru) */
 };
 
 typedef struct {
@@ -365,6 +371,33 @@ typedef struct {
 int atp_load_weights(const atp_plan_t *plan, const atp_st_t *st, const char *const *names,
                      int32_t n_names, void *inflow_host, uint64_t inflow_bytes,
                      int32_t n_threads, atp_load_stats *stats);
+
+/* ---- KV budget under recovery (Sec. III-A: per-session recency; cold KV
+ * released least recently used first when the demand exceeds the budget,
+ * evicted sessions being rebuilt later by replay) ----------------------- */
+typedef struct {
+  int32_t kept_sessions, evicted_sessions;
+  int64_t live_before, live_after;      /* distinct live block ids          */
+  uint64_t demand_before, demand_after; /* live blocks x block_bytes        */
+} atp_evict_stats;
+
+/* Choose the sessions (rows of a host block table [n_seq][max_blocks], -1 =
+ * unused, ids < num_blocks) that the new layout keeps under `budget_bytes`:
+ *   last_use     per-session last-use time; larger = more recent
+ *   block_bytes  bytes one block occupies in the new layout over all layers,
+ *                K and V (stats.new_kv_bytes / num_blocks)
+ * Sessions are evicted in ascending (last_use, session index) order while
+ * (distinct live ids of the kept rows) x block_bytes > budget_bytes; a block
+ * several rows share stays until its last row goes.  Outputs keep[n_seq]
+ * (1 kept, 0 evicted) and new_table (may alias table): evicted rows become
+ * all -1; with `compact` nonzero every kept id p becomes its rank among the
+ * kept ids, the numbering of an ATP_KV_COMPACT arena.  Build the plan with
+ * kv.live_blocks = stats.live_after and pass the kept rows (ids unchanged,
+ * i.e. the table with compact = 0) to atp_reshard_kv.  ATP_EINVAL on an id
+ * outside [-1, num_blocks) or NULL arrays. */
+int atp_kv_evict_lru(const int32_t *table, int32_t n_seq, int32_t max_blocks, int64_t num_blocks,
+                     const int64_t *last_use, uint64_t block_bytes, uint64_t budget_bytes,
+                     int32_t compact, int32_t *keep, int32_t *new_table, atp_evict_stats *stats);
 
 const char *atp_last_error(void);
 

@@ -219,6 +219,16 @@ def kv_arena(pb: Problem, content, table, pool: int, which: str, poison: int = 0
     return arena
 
 
+def kv_arena_compact(pb: Problem, content, table, pool: int, which: str = "new") -> np.ndarray:
+    """The KV arena indexed by block rank instead of block id: in each
+    (layer, K|V) plane, position r holds the live block whose id is the r-th
+    smallest (a compact pool of exactly the live blocks)."""
+    by_id = kv_arena(pb, content, table, pool, which)
+    live = live_blocks(table)
+    planes = by_id.reshape(2 * pb.n_layers, pool, -1)
+    return np.ascontiguousarray(planes[:, live, :]).reshape(-1)
+
+
 def packed_kv_inflow(pb: Problem, content, table, pool: int) -> np.ndarray:
     new_arena = kv_arena(pb, content, table, pool, "new")
     live = live_blocks(table)

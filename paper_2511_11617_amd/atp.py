@@ -26,6 +26,7 @@ ASSIGN_INORDER, ASSIGN_MAXRETAIN = 0, 1
 INPLACE = 1 << 4
 PLAN_GREEDY = 1 << 8
 PLAN_FULL = 1 << 9
+KV_COMPACT = 1 << 10
 KEEP, P2P, RELOAD = 0, 1, 2
 SEG_INFLOW_W, SEG_OUTBOUND_W, SEG_INFLOW_KV, SEG_OUTBOUND_KV = 0, 1, 2, 3
 
@@ -34,6 +35,7 @@ EXPORTS = [
     "atp_plan_stats", "atp_plan_tasks", "atp_plan_ranges", "atp_plan_owner",
     "atp_plan_layout", "atp_plan_segments", "atp_plan_launches", "atp_partition",
     "atp_last_error", "atp_st_open", "atp_st_close", "atp_st_find", "atp_load_weights",
+    "atp_kv_evict_lru",
 ]
 
 
@@ -106,6 +108,12 @@ class StTensor(C.Structure):
                 ("shape", C.c_int64 * 8), ("offset", C.c_uint64), ("bytes", C.c_uint64)]
 
 
+class EvictStats(C.Structure):
+    _fields_ = [("kept_sessions", C.c_int32), ("evicted_sessions", C.c_int32),
+                ("live_before", C.c_int64), ("live_after", C.c_int64),
+                ("demand_before", C.c_uint64), ("demand_after", C.c_uint64)]
+
+
 class LoadStats(C.Structure):
     _fields_ = [("read_ms", C.c_double), ("bytes", C.c_uint64), ("reads", C.c_uint64),
                 ("tensor_bytes", C.c_uint64), ("threads", C.c_int32)]
@@ -159,6 +167,8 @@ def _load():
     lib.atp_st_find.argtypes = [P, C.c_char_p, C.POINTER(StTensor)]
     lib.atp_load_weights.argtypes = [P, P, C.POINTER(C.c_char_p), C.c_int32, P, C.c_uint64, C.c_int32,
                                      C.POINTER(LoadStats)]
+    lib.atp_kv_evict_lru.argtypes = [P, C.c_int32, C.c_int32, C.c_int64, P, C.c_uint64, C.c_uint64, C.c_int32,
+                                     P, P, C.POINTER(EvictStats)]
     lib.atp_last_error.restype = C.c_char_p
     for f in EXPORTS:
         if f not in ("atp_plan_free", "atp_last_error", "atp_st_close"):
@@ -266,6 +276,24 @@ class Plan:
         _check(lib.atp_load_weights(self.h, files.h, arr, len(names), inflow, inflow_bytes, threads,
                                     C.byref(st)))
         return st
+
+
+def kv_evict_lru(table, last_use, num_blocks: int, block_bytes: int, budget_bytes: int, compact=False):
+    """LRU session eviction under a KV budget (atp_kv_evict_lru).
+    table: int32 [n_seq, max_blocks]; last_use: int64 [n_seq].
+    Returns (keep bool array, new table, EvictStats)."""
+    import numpy as np
+    t = np.ascontiguousarray(table, dtype=np.int32)
+    lu = np.ascontiguousarray(last_use, dtype=np.int64)
+    if lu.shape != (t.shape[0],):
+        raise ValueError("last_use needs one entry per session")
+    keep = np.zeros(t.shape[0], np.int32)
+    out = np.empty_like(t)
+    st = EvictStats()
+    _check(lib.atp_kv_evict_lru(t.ctypes.data, t.shape[0], t.shape[1], num_blocks, lu.ctypes.data, block_bytes,
+                                budget_bytes, int(bool(compact)), keep.ctypes.data, out.ctypes.data,
+                                C.byref(st)))
+    return keep.astype(bool), out, st
 
 
 class StFiles:

@@ -8,6 +8,7 @@
 
 #include "../../include/atp.h"
 #include "exec.h"
+#include "kvbudget.h"
 #include "loader.h"
 #include "plan.h"
 
@@ -296,6 +297,16 @@ int atp_load_weights(const atp_plan_t *plan, const atp_st_t *st, const char *con
   return guard([&]() -> int {
     if (!plan || !st) return fail(ATP_EINVAL, "plan or st is NULL");
     atp::load_weights(*plan->p, *st->f, names, n_names, inflow_host, inflow_bytes, n_threads, stats);
+    return ATP_OK;
+  });
+}
+
+int atp_kv_evict_lru(const int32_t *table, int32_t n_seq, int32_t max_blocks, int64_t num_blocks,
+                     const int64_t *last_use, uint64_t block_bytes, uint64_t budget_bytes, int32_t compact,
+                     int32_t *keep, int32_t *new_table, atp_evict_stats *stats) {
+  return guard([&]() -> int {
+    atp::evict_lru(table, n_seq, max_blocks, num_blocks, last_use, block_bytes, budget_bytes, compact != 0, keep,
+                   new_table, stats);
     return ATP_OK;
   });
 }

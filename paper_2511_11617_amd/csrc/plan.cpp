@@ -473,11 +473,15 @@ void lower_kv(Plan &P, std::vector<Fam> &retained, std::vector<Pending> &inflow,
   uint64_t eb = kv.elem_bytes, bt = kv.block_tokens, hd = kv.head_dim;
   uint64_t nb = kv.num_blocks, live = kv.live_blocks;
   bool tok = kv.layout == ATP_KV_TOKEN_MAJOR;
+  // compact: the new planes hold the live blocks only, each at its rank
+  const bool compact = P.flags & ATP_KV_COMPACT;
+  const uint64_t nb_new = compact ? live : nb;
+  const uint32_t dst_ind = compact ? 0u : uint32_t(DF_DST_IND);
   uint64_t hb = bt * hd * eb;                  // one head of one block
   uint64_t obs = uint64_t(ho.e - ho.b) * hb;   // old block bytes
   uint64_t nbs = uint64_t(hn.e - hn.b) * hb;   // new block bytes
   c.old_bytes = uint64_t(kv.num_layers) * 2 * nb * obs;
-  c.new_bytes = uint64_t(kv.num_layers) * 2 * nb * nbs;
+  c.new_bytes = uint64_t(kv.num_layers) * 2 * nb_new * nbs;
   // a head range [a, b) of a block, in a block whose heads start at h0
   auto side = [&](uint64_t base, uint64_t block_bytes, int64_t h0, int64_t nh, int64_t a, int64_t b, Fam &f,
                   bool src) {
@@ -509,7 +513,7 @@ void lower_kv(Plan &P, std::vector<Fam> &retained, std::vector<Pending> &inflow,
   for (int l = 0; l < kv.num_layers; ++l) {
     for (int which = 0; which < 2; ++which) {
       uint64_t g = uint64_t(l) * 2 + which;
-      uint64_t obase = g * nb * obs, nbase = g * nb * nbs;
+      uint64_t obase = g * nb * obs, nbase = g * nb_new * nbs;
       for (const atp_task &x : sp.tasks) {
         if (x.dst != P.self_new) continue;
         Fam f;
@@ -517,7 +521,7 @@ void lower_kv(Plan &P, std::vector<Fam> &retained, std::vector<Pending> &inflow,
         uint64_t bytes = live * f.rows * f.run;
         if (x.kind == ATP_KEEP) {
           side(obase, obs, ho.b, ho.e - ho.b, x.begin, x.end, f, true);
-          f.flags = bufs(BUF_IN, BUF_OUT) | DF_SRC_IND | DF_DST_IND;
+          f.flags = bufs(BUF_IN, BUF_OUT) | DF_SRC_IND | dst_ind;
           if (P.inplace) {
             f.flags |= DF_BLOCKRANGE;
             f.o_begin = 0;
@@ -534,7 +538,7 @@ void lower_kv(Plan &P, std::vector<Fam> &retained, std::vector<Pending> &inflow,
           f.src_ostride = f.rows * f.run;
           f.o_begin = 0;
           f.o_end = int64_t(live);
-          f.flags = bufs(BUF_STAGE, BUF_OUT) | DF_DST_IND;
+          f.flags = bufs(BUF_STAGE, BUF_OUT) | dst_ind;
           if (live) inflow.push_back({f, cur_in, false});
           atp_segment sg{-1, l, which, x.kind, x.begin, x.end, cur_in, bytes};
           c.seg_in.push_back(sg);
@@ -1207,6 +1211,8 @@ Plan *make_plan(const atp_problem *p) {
   P->prob = *p;
   P->flags = p->flags;
   P->inplace = p->flags & ATP_INPLACE;
+  // the in-place schedule relies on block ids that stay put
+  if (P->inplace && (p->flags & ATP_KV_COMPACT)) fail(ATP_EINVAL, "ATP_KV_COMPACT needs an out-of-place reshard");
   resolve_spaces(*P);
   if (p->self_old_rank < 0 || p->self_old_rank >= P->sp[0].N) fail(ATP_EINVAL, "self_old_rank out of range");
   P->self_old = p->self_old_rank;  // shard geometry below is this rank's

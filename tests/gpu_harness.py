@@ -13,7 +13,7 @@ import sys
 import numpy as np
 import torch
 
-from oracle import model, repack
+from oracle import kvbudget, model, repack
 from paper_2511_11617_amd import atp, problem
 from synth import pagetable
 from synth.content import KIND_FP16, Content
@@ -44,26 +44,40 @@ def say(msg):
 
 
 def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
-             ckpt_dir=None):
+             ckpt_dir=None, evict=None):
     """Reshard one workload on the GPU and compare with the oracle.  With
     `ckpt_dir`, the weight inflow is read from a safetensors checkpoint
     written there by the library's range-read loader instead of being copied
-    from the oracle's packed inflow."""
+    from the oracle's packed inflow.  With `evict` = (last_use, budget
+    fraction of the new KV demand), the oracle's LRU policy picks the kept
+    sessions; the old arena holds every session, the reshard gets the kept
+    rows, and with ATP_KV_COMPACT the result is the oracle's compact arena."""
     say(f"[gpu case] {name} cfg={c.get('name', '?')} layers={c['layers']} flags={flags} "
         f"old_tp={c['old_tp']} new_tp={c['new_tp']} failed={c['failed']} self_old={c['self_old']}")
     pb = model.build(c, assign=assign, variant=variant)
     content = CachedContent(Content(c["seed"], c["w_kind"], c["kv_kind"]))
     table, pool = pagetable.make_for(c)
+    full_table = table
+    if evict is not None:
+        last_use, frac = evict
+        bb = pb.kv_arena_bytes("new", pool) // pool
+        keep = kvbudget.lru_keep(table, last_use, bb, int(frac * len(repack.live_blocks(table)) * bb))
+        table = kvbudget.evicted_table(table, keep, compact=False)
     n_live = int(len(repack.live_blocks(table)))
     inplace = bool(flags & atp.INPLACE)
+    compact = bool(flags & atp.KV_COMPACT)
 
     old_w = repack.weight_arena(pb, content, "old")
     want_w = repack.weight_arena(pb, content, "new")
     mask_w = repack.weight_live_mask(pb, "new")
     in_w = repack.packed_weight_inflow(pb, content)
-    old_k = repack.kv_arena(pb, content, table, pool, "old", poison=0xDEAD)
-    want_k = repack.kv_arena(pb, content, table, pool, "new")
-    mask_k = repack.kv_live_mask(pb, table, pool, "new")
+    old_k = repack.kv_arena(pb, content, full_table, pool, "old", poison=0xDEAD)
+    if compact:
+        want_k = repack.kv_arena_compact(pb, content, table, pool)
+        mask_k = np.ones(want_k.size, bool)
+    else:
+        want_k = repack.kv_arena(pb, content, table, pool, "new")
+        mask_k = repack.kv_live_mask(pb, table, pool, "new")
     in_k = repack.packed_kv_inflow(pb, content, table, pool)
 
     b = problem.build(c, n_live=n_live, pool=pool, flags=flags, staging_cap=staging_cap)
