@@ -7,9 +7,9 @@
 //                 blocks (wavefront prefix sums over block flags), resolves
 //                 block-id ranges into list positions and scans the tile
 //                 counts of every descriptor (wavefront prefix sums).
-//   k_copy16      descriptor-driven copy in 16-byte chunks, 8 independent
+//   k_copy16      descriptor-driven copy in 16-byte chunks, 2 independent
 //                 loads in flight per thread, non-temporal hints; a tile is
-//                 2048 consecutive chunks of one descriptor.
+//                 512 consecutive chunks (8 KiB) of one descriptor.
 //   k_copy_bytes  the same for runs that are not 16-byte aligned (odd
 //                 column counts): a tile stages one 8 KiB line segment in
 //                 LDS with aligned 16-byte loads and writes it out with
@@ -170,21 +170,51 @@ struct LineAddr {
   char *src, *dst;
 };
 
+// The live-block list and the descriptors are never written while a copy
+// kernel runs, so a wave-uniform index may read them through the scalar
+// cache (constant address space) instead of a per-lane vector load.
+typedef const int32_t __attribute__((address_space(4))) *const_i32_p;
+
+// Addresses of line `line` of descriptor x.  UNIFORM: `line` is the same on
+// every lane of the wave, and the block id comes in through a scalar load.
+template <bool UNIFORM>
+__device__ __forceinline__ LineAddr line_addr(const Desc &x, uint32_t line, char *b0, char *b1, char *b2,
+                                              const int32_t *__restrict__ live) {
+  uint32_t orel = divq(line, x.magic_rows);
+  uint32_t r = line - orel * x.rows;
+  int64_t o = x.o_begin + orel;
+  uint64_t id = 0;
+  if (x.flags & (DF_SRC_IND | DF_DST_IND))
+    id = UNIFORM ? uint64_t(((const_i32_p)(live))[o]) : uint64_t(live[o]);
+  uint64_t si = (x.flags & DF_SRC_IND) ? id : uint64_t(orel);
+  uint64_t di = (x.flags & DF_DST_IND) ? id : uint64_t(orel);
+  char *sb = slot_base((x.flags >> DF_SRC_SHIFT) & 3, b0, b1, b2);
+  char *db = slot_base((x.flags >> DF_DST_SHIFT) & 3, b0, b1, b2);
+  LineAddr la;
+  la.src = sb + x.src_off + si * x.src_ostride + uint64_t(r) * x.src_pitch;
+  la.dst = db + x.dst_off + di * x.dst_ostride + uint64_t(r) * x.dst_pitch;
+  return la;
+}
+
 // Streaming 16-byte accesses: nothing is read twice, so both sides carry
-// the non-temporal hint by default.
+// the non-temporal hint by default.  The pointers are cast to the global
+// address space, which keeps the accesses global_* rather than flat_*
+// where the compiler cannot infer it.
+typedef u32x4 __attribute__((address_space(1))) global_u32x4;
+
 __device__ __forceinline__ u32x4 load16(const u32x4 *p) {
 #if ATP_NT_LOAD
-  return __builtin_nontemporal_load(p);
+  return __builtin_nontemporal_load((const global_u32x4 *)(p));
 #else
-  return *p;
+  return *(const global_u32x4 *)(p);
 #endif
 }
 
 __device__ __forceinline__ void store16(u32x4 *p, u32x4 v) {
 #if ATP_NT_STORE
-  __builtin_nontemporal_store(v, p);
+  __builtin_nontemporal_store(v, (global_u32x4 *)(p));
 #else
-  *p = v;
+  *(global_u32x4 *)(p) = v;
 #endif
 }
 
@@ -200,28 +230,18 @@ __device__ __forceinline__ int64_t tile_of_block() {
 #endif
 }
 
-__device__ __forceinline__ LineAddr line_addr(const Desc &x, uint32_t line, char *b0, char *b1, char *b2,
-                                              const int32_t *__restrict__ live) {
-  uint32_t orel = divq(line, x.magic_rows);
-  uint32_t r = line - orel * x.rows;
-  int64_t o = x.o_begin + orel;
-  uint64_t si = (x.flags & DF_SRC_IND) ? uint64_t(live[o]) : uint64_t(orel);
-  uint64_t di = (x.flags & DF_DST_IND) ? uint64_t(live[o]) : uint64_t(orel);
-  char *sb = slot_base((x.flags >> DF_SRC_SHIFT) & 3, b0, b1, b2);
-  char *db = slot_base((x.flags >> DF_DST_SHIFT) & 3, b0, b1, b2);
-  LineAddr la;
-  la.src = sb + x.src_off + si * x.src_ostride + uint64_t(r) * x.src_pitch;
-  la.dst = db + x.dst_off + di * x.dst_ostride + uint64_t(r) * x.dst_pitch;
-  return la;
-}
-
+// Each tile resolves every address first (descriptor by value, block ids
+// through scalar loads), then issues all of its loads, then all stores, so
+// that no load waits behind another's address computation.  Lanes past the
+// end of the tile load its last chunk again (a valid address) and store
+// nothing: unconditional loads keep the compiler from waiting on each one.
 __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ descs, const int64_t *__restrict__ prefix,
                                                      int d0, int d1, char *b0, char *b1, char *b2,
                                                      const int32_t *__restrict__ live) {
   const int64_t T0 = prefix[d0], T1 = prefix[d1];
   for (int64_t t = T0 + tile_of_block(); t < T1; t += gridDim.x) {
     const int d = find_desc(prefix, d0, d1, t);
-    const Desc &x = descs[d];
+    const Desc x = descs[d];
     const uint32_t cpl = x.run >> 4;
     const uint64_t total = uint64_t(x.o_end - x.o_begin) * x.rows * cpl;
     const uint64_t cbase = uint64_t(t - prefix[d]) * kTileChunks;
@@ -230,7 +250,7 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
     u32x4 v[kUnroll];
     if (l0 == divq(uint32_t(clast), x.magic_line)) {
       // the whole tile lies in one line: one address computation per tile
-      const LineAddr la = line_addr(x, l0, b0, b1, b2, live);
+      const LineAddr la = line_addr<true>(x, l0, b0, b1, b2, live);
       const uint32_t col0 = uint32_t(cbase) - l0 * cpl;
       const uint32_t n = uint32_t(clast - cbase) + 1;
       const u32x4 *s = reinterpret_cast<const u32x4 *>(la.src) + col0;
@@ -238,7 +258,7 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
 #pragma unroll
       for (int k = 0; k < kUnroll; ++k) {
         const uint32_t i = threadIdx.x + k * kThreads;
-        if (i < n) v[k] = load16(s + i);
+        v[k] = load16(s + (i < n ? i : n - 1));
       }
 #pragma unroll
       for (int k = 0; k < kUnroll; ++k) {
@@ -249,34 +269,35 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
     }
     // several lines per tile: resolve the line once per wavefront when its
     // 64 chunks share one (short KV head runs), else per lane
+    const u32x4 *sp[kUnroll];
     u32x4 *dp[kUnroll];
     const uint32_t wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
-      const uint64_t g0 = cbase + uint64_t(k) * kThreads + wv * 64;
-      const uint64_t c = cbase + threadIdx.x + uint64_t(k) * kThreads;
-      dp[k] = nullptr;
-      if (g0 > clast) continue;
-      const uint64_t gl = g0 + 63 < clast ? g0 + 63 : clast;
+      const uint64_t g0r = cbase + uint64_t(k) * kThreads + wv * 64;
+      const uint64_t g0 = g0r < clast ? g0r : clast;
+      const uint64_t gl = g0r + 63 < clast ? g0r + 63 : clast;
+      const uint64_t cr = cbase + threadIdx.x + uint64_t(k) * kThreads;
+      const uint64_t c = cr < clast ? cr : clast;
       const uint32_t lf = divq(uint32_t(g0), x.magic_line);
       if (lf == divq(uint32_t(gl), x.magic_line)) {
-        const LineAddr la = line_addr(x, lf, b0, b1, b2, live);
+        const LineAddr la = line_addr<true>(x, lf, b0, b1, b2, live);
         const uint32_t col = uint32_t(c) - lf * cpl;
-        if (c <= clast) {
-          v[k] = load16(reinterpret_cast<const u32x4 *>(la.src) + col);
-          dp[k] = reinterpret_cast<u32x4 *>(la.dst) + col;
-        }
-      } else if (c <= clast) {
+        sp[k] = reinterpret_cast<const u32x4 *>(la.src) + col;
+        dp[k] = reinterpret_cast<u32x4 *>(la.dst) + col;
+      } else {
         const uint32_t line = divq(uint32_t(c), x.magic_line);
         const uint32_t col = uint32_t(c) - line * cpl;
-        LineAddr la = line_addr(x, line, b0, b1, b2, live);
-        v[k] = load16(reinterpret_cast<const u32x4 *>(la.src) + col);
+        const LineAddr la = line_addr<false>(x, line, b0, b1, b2, live);
+        sp[k] = reinterpret_cast<const u32x4 *>(la.src) + col;
         dp[k] = reinterpret_cast<u32x4 *>(la.dst) + col;
       }
     }
 #pragma unroll
+    for (int k = 0; k < kUnroll; ++k) v[k] = load16(sp[k]);
+#pragma unroll
     for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) store16(dp[k], v[k]);
+      if (cbase + threadIdx.x + uint64_t(k) * kThreads <= clast) store16(dp[k], v[k]);
   }
 }
 
@@ -288,12 +309,12 @@ __global__ void __launch_bounds__(kThreads) k_copy_bytes(const Desc *__restrict_
   const int tid = threadIdx.x;
   for (int64_t t = T0 + blockIdx.x; t < T1; t += gridDim.x) {
     const int d = find_desc(prefix, d0, d1, t);
-    const Desc &x = descs[d];
+    const Desc x = descs[d];
     const uint32_t spl = uint32_t((x.run + kSegBytes - 1) / kSegBytes);
     const uint32_t tin = uint32_t(t - prefix[d]);
     const uint32_t line = divq(tin, x.magic_line);
     const uint32_t seg = tin - line * spl;
-    LineAddr la = line_addr(x, line, b0, b1, b2, live);
+    LineAddr la = line_addr<true>(x, line, b0, b1, b2, live);
     const uint64_t skip = uint64_t(seg) * kSegBytes;
     const char *src = la.src + skip;
     char *dst = la.dst + skip;
