@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 # counters read for a plain 4 GiB copy: x2.0 and x1.0), valid only while the
 # kernel sources hash to `src`.
 COUNTED_TRAFFIC = {
-    "src": "59284d6e159d213b",
-    "dense-40L-h5120-tp4to3": {"kv": 10738027520, "weights": 9080776704},
+    "src": "d9999845543f9207",
+    "dense-40L-h5120-tp4to3": {"kv": 10738045781, "weights": 9069669589},
 }
 
 
