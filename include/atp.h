@@ -170,6 +170,10 @@ void atp_plan_free(atp_plan_t *plan);
  *                (in place only) the old bytes peers need and this GPU drops,
  *                read before they are overwritten; may be NULL if 0 bytes
  *   staging      device scratch of at least stats.staging_w bytes
+ * With ATP_INPLACE the copy kernel itself reads the inflow that must wait
+ * for a level or an outbound read: inflow_host must then come from
+ * hipHostMalloc (device-accessible at the same address) and be 256-byte
+ * aligned, else ATP_EINVAL / ATP_EALIGN.
  * Launch errors return ATP_EHIP; kernel-side errors surface in atp_sync. */
 int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes,
                         void *new_arena, uint64_t new_arena_bytes,
@@ -210,6 +214,10 @@ typedef struct {
   uint64_t h2d_bytes, d2h_bytes, scatter_bytes;
   int32_t n_launches;
   int32_t reserved;
+  double repack_union_ms; /* time during which any repack kernel of the
+                             pending calls ran (their intervals' union):
+                             the device repack time when the weights and
+                             KV repacks overlap                          */
 } atp_timing;
 
 /* Wait for the pending reshard calls of `plan`; returns the first
@@ -271,8 +279,9 @@ int atp_plan_segments(const atp_plan_t *plan, int32_t which, atp_segment *out,
                       int32_t cap, int32_t *n);
 
 /* One kernel launch of the last reshard: kind 0 = weight repack,
- * 1 = KV repack, 2 = scatter, 3 = staging copy; `ms` from HIP events on
- * the compute stream. */
+ * 1 = KV repack, 2 = landing-ring scatter, 3 = outbound gather into
+ * staging (in place), 4 = inflow read from the host buffer (in place);
+ * `ms` from HIP events on the stream the launch ran on. */
 typedef struct {
   int32_t kind, level;
   uint64_t bytes;
@@ -287,7 +296,8 @@ int atp_plan_launches(const atp_plan_t *plan, atp_launch *out, int32_t cap, int3
  *   H2D_RING host inflow -> landing-ring slot (staging), then the SCATTER
  *            copies that follow it; ring traffic starts after all levels
  *   H2D      host inflow -> arena, allowed once level `level` has
- *            finished (level -1: at any time)
+ *            finished (level -1: at any time) and the first `after_d2h`
+ *            D2H copies of the list have finished
  *   D2H      arena or staging -> host outbound buffer; must finish
  *            before level `level` starts (-1: before any inflow landing
  *            that waits for it); issued one after another in list order

@@ -75,7 +75,7 @@ class Timing(C.Structure):
                 ("repack_kv_ms", C.c_double), ("repack_span_ms", C.c_double), ("h2d_ms", C.c_double), ("d2h_ms", C.c_double),
                 ("scatter_ms", C.c_double), ("overlap", C.c_double), ("repack_bytes", C.c_uint64),
                 ("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("scatter_bytes", C.c_uint64),
-                ("n_launches", C.c_int32), ("reserved", C.c_int32)]
+                ("n_launches", C.c_int32), ("reserved", C.c_int32), ("repack_union_ms", C.c_double)]
 
 
 class Stats(C.Structure):

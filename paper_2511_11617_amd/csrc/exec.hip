@@ -3,16 +3,19 @@
 // buffer, launches the prepare and repack kernels level by level on the
 // compute stream, lands the missing bytes from the pinned host buffer on the
 // copy stream (directly, or through the landing ring plus a scatter kernel),
-// reads dropped outbound bytes out before an in-place overwrite, and orders
-// the three with HIP events.
+// reads dropped outbound bytes out before an in-place overwrite (on a side
+// stream that feeds a hardware queue of its own), and orders them with HIP
+// events.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <chrono>
 #include <map>
 #include <mutex>
+#include <cstdio>
 #include <cstring>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "exec.h"
@@ -56,7 +59,8 @@ struct CallState {
 // every plan would otherwise cost tens of milliseconds per reshard.
 struct DevicePool {
   std::vector<hipEvent_t> sync_ev, time_ev;
-  std::vector<hipStream_t> streams;
+  std::vector<hipStream_t> streams;  // side-stream candidates that did not qualify: kept alive, so
+                                     // that no new stream reuses a handle the probe cache knows
   std::vector<std::pair<void *, size_t>> pinned;
 };
 std::mutex g_pool_mu;
@@ -65,9 +69,12 @@ std::map<int, DevicePool> g_pools;
 struct Exec {
   int device = -1;
   int grid_max = 2048;
-  hipStream_t d2h = nullptr;    // outbound reads (in place)
-  hipStream_t copy2 = nullptr;  // in-place weight landings that wait for levels / outbound reads
-  hipStream_t comp2 = nullptr;  // in-place weight levels and scatters
+  // In place: `side` runs the outbound gathers and their device-to-host
+  // copies, the weight levels that wait for them and the weight inflow the
+  // copy kernel reads after them.  It feeds another hardware queue than the
+  // caller's streams and is shared process-wide (choose_side).
+  hipStream_t side = nullptr;
+  hipStream_t side_for_compute = nullptr, side_for_copy = nullptr;
   std::vector<hipEvent_t> sync_pool, time_pool;
   size_t sync_used = 0, time_used = 0;
   CallState w, k;
@@ -108,20 +115,6 @@ struct Exec {
     }
     return time_pool[time_used++];
   }
-  hipStream_t stream() {
-    {
-      std::lock_guard<std::mutex> g(g_pool_mu);
-      auto &v = g_pools[device].streams;
-      if (!v.empty()) {
-        hipStream_t s = v.back();
-        v.pop_back();
-        return s;
-      }
-    }
-    hipStream_t s;
-    HIPCHK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));  // default priority
-    return s;
-  }
   void *pinned(size_t bytes, size_t *cap) {
     {
       std::lock_guard<std::mutex> g(g_pool_mu);
@@ -149,8 +142,6 @@ struct Exec {
       if (c->desc_host) pl.pinned.push_back({c->desc_host, c->desc_cap * sizeof(Desc)});
       if (c->err_host) pl.pinned.push_back({c->err_host, 256});
     }
-    for (hipStream_t st : {d2h, copy2, comp2})
-      if (st) pl.streams.push_back(st);
   }
 };
 
@@ -164,6 +155,117 @@ Exec &exec_of(Plan &P) {
     P.exec = e;
   }
   return *static_cast<Exec *>(P.exec);
+}
+
+// ---- hardware queues -------------------------------------------------------------
+// HIP feeds every stream of a process into one of a few hardware queues (four
+// by default), and a queue runs its commands in order whichever stream they
+// came from.  A stream that waits for 200 ms of outbound reads therefore
+// stalls every other stream on its queue.  Whether two streams share a queue
+// is observed directly: an empty kernel on `b` finishes before a bounded
+// spin kernel queued on `a` ends only if the two queues differ.
+
+__global__ void k_spin(uint32_t iters) {
+  for (uint32_t i = 0; i < iters; ++i) __builtin_amdgcn_s_sleep(127);  // about 8 K clocks each
+}
+__global__ void k_nop() {}
+
+constexpr uint32_t kSpinIters = 400;     // about 1.4 ms at 2.4 GHz
+constexpr float kSpinMarginMs = 0.3f;    // the empty kernel must finish this much earlier
+constexpr int kSideCandidates = 8;       // streams tried before giving up on a free queue
+
+// Workgroups of the host-read launches (a persistent grid over their
+// tiles): 64 already carry a full x16 Gen5 link from pinned host memory.
+constexpr uint64_t kHostReadGrid = 128;
+std::map<std::pair<hipStream_t, hipStream_t>, bool> g_same_queue;  // under g_pool_mu
+
+bool same_queue(Exec &E, hipStream_t a, hipStream_t b) {
+  if (a == b) return true;
+  {
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    auto it = g_same_queue.find({a, b});
+    if (it != g_same_queue.end()) return it->second;
+  }
+  hipEvent_t ea = E.ev_time(), eb = E.ev_time();
+  hipLaunchKernelGGL(k_spin, dim3(1), dim3(64), 0, a, kSpinIters);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipEventRecord(ea, a));
+  hipLaunchKernelGGL(k_nop, dim3(1), dim3(64), 0, b);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipEventRecord(eb, b));
+  HIPCHK(hipEventSynchronize(ea));
+  HIPCHK(hipEventSynchronize(eb));
+  float ms = 0;
+  HIPCHK(hipEventElapsedTime(&ms, eb, ea));  // spin end minus empty-kernel end
+  const bool same = ms < kSpinMarginMs;
+  std::lock_guard<std::mutex> g(g_pool_mu);
+  g_same_queue[{a, b}] = g_same_queue[{b, a}] = same;
+  return same;
+}
+
+// The side stream for a pair of caller streams: one on a hardware queue that
+// neither caller stream uses, chosen once per (device, compute, copy) and
+// shared by every plan (work from several plans on it is merely serialised).
+// At most kSideCandidates streams are ever created for a pair; when none of
+// them qualifies, the first is used and the outbound work then holds up the
+// caller's stream on that queue (the reshard stays correct).
+std::map<std::tuple<int, hipStream_t, hipStream_t>, hipStream_t> g_side;  // under g_pool_mu
+
+void choose_side(Exec &E, hipStream_t compute, hipStream_t copy) {
+  if (E.side && E.side_for_compute == compute && E.side_for_copy == copy) return;
+  const auto key = std::make_tuple(E.device, compute, copy);
+  {
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    auto it = g_side.find(key);
+    if (it != g_side.end()) {
+      E.side = it->second;
+      E.side_for_compute = compute;
+      E.side_for_copy = copy;
+      return;
+    }
+  }
+  std::vector<hipStream_t> made;
+  hipStream_t pick = nullptr;
+  for (int i = 0; i < kSideCandidates && !pick; ++i) {
+    hipStream_t s = nullptr;
+    HIPCHK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));  // default priority
+    made.push_back(s);
+    if (!same_queue(E, compute, s) && !same_queue(E, copy, s)) pick = s;
+  }
+  if (!pick) {
+    pick = made.front();
+    fprintf(stderr, "atp: no hardware queue free of the caller's streams after %d tries; the in-place "
+                    "outbound work shares one\n", kSideCandidates);
+  }
+  {
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    auto &pool = g_pools[E.device].streams;
+    for (hipStream_t s : made)
+      if (s != pick) pool.push_back(s);
+    auto ins = g_side.insert({key, pick});
+    E.side = ins.first->second;  // another thread may have chosen first
+  }
+  E.side_for_compute = compute;
+  E.side_for_copy = copy;
+}
+
+// The copy kernel reads or writes a host buffer only through its device
+// address; memory not pinned by HIP would fault the GPU, so it is refused.
+void check_kernel_host_buffer(const void *p, uint64_t bytes, const char *what) {
+  if (!bytes) return;
+  if (!p) throw Error(ATP_EINVAL, std::string(what) + " is NULL");
+  if (reinterpret_cast<uintptr_t>(p) % 256)
+    throw Error(ATP_EALIGN, std::string(what) + " must be 256-byte aligned for an in-place reshard");
+  for (const char *q : {static_cast<const char *>(p), static_cast<const char *>(p) + bytes - 1}) {
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, q) != hipSuccess || a.type != hipMemoryTypeHost || a.hostPointer == nullptr ||
+        a.devicePointer != a.hostPointer) {
+      (void)hipGetLastError();
+      throw Error(ATP_EINVAL, std::string(what) +
+                                  " must be pinned host memory from hipHostMalloc for an in-place reshard "
+                                  "(the copy kernel accesses it directly)");
+    }
+  }
 }
 
 void build_descs(Exec &E, const CallPlan &c, CallState &cs) {
@@ -212,13 +314,31 @@ uint64_t extent(const Fam &f, bool src, int64_t n_blocks, int64_t live) {
 }
 
 void check_extents(const CallPlan &c, bool kvcall, const Plan &P, uint64_t in_bytes, uint64_t out_bytes,
-                   uint64_t stage_bytes) {
+                   uint64_t stage_bytes, uint64_t inflow_bytes, uint64_t outbound_bytes) {
   int64_t nb = kvcall ? P.kv.num_blocks : 0, live = kvcall ? P.kv.live_blocks : 0;
-  for (const Fam &f : c.fams) {
+  // the host-read launches bind slot IN to the pinned inflow buffer
+  const int h0 = c.host_reads.empty() ? -1 : c.host_reads.front().d0;
+  const int h1 = c.host_reads.empty() ? -1 : c.host_reads.back().d1;
+  auto fits = [](uint64_t off, uint64_t bytes, uint64_t lim) { return bytes <= lim && off <= lim - bytes; };
+  for (const HostCopy &h : c.directs)
+    if (!fits(h.host_off, h.bytes, inflow_bytes) || !fits(h.dev_off, h.bytes, out_bytes))
+      throw Error(ATP_ECAPACITY, "an inflow landing would run past the end of a buffer");
+  for (const Chunk &ch : c.chunks)
+    for (const HostCopy &h : ch.copies)
+      if (!fits(h.host_off, h.bytes, inflow_bytes) || !fits(h.dev_off, h.bytes, stage_bytes))
+        throw Error(ATP_ECAPACITY, "an inflow landing would run past the end of a buffer");
+  for (const OutChunk &ch : c.out_chunks)
+    for (const HostCopy &h : ch.d2h)
+      if (!fits(h.host_off, h.bytes, outbound_bytes) || !fits(h.dev_off, h.bytes, stage_bytes))
+        throw Error(ATP_ECAPACITY, "an outbound copy would run past the end of a buffer");
+  for (int d = 0; d < int(c.fams.size()); ++d) {
+    const Fam &f = c.fams[size_t(d)];
+    const bool host_read = d >= h0 && d < h1;
     for (int side = 0; side < 2; ++side) {
       uint32_t slot = (f.flags >> (side == 0 ? DF_SRC_SHIFT : DF_DST_SHIFT)) & 3;
       uint64_t e = extent(f, side == 0, nb, live);
       uint64_t lim = slot == BUF_IN ? in_bytes : slot == BUF_OUT ? out_bytes : stage_bytes;
+      if (host_read && slot == BUF_IN) lim = inflow_bytes;
       if (e > lim) throw Error(ATP_ECAPACITY, "a copy would run past the end of a buffer");
     }
     uint64_t lines = uint64_t(kvcall ? std::max<int64_t>(nb, f.o_end - f.o_begin) : f.o_end - f.o_begin) * f.rows;
@@ -227,9 +347,10 @@ void check_extents(const CallPlan &c, bool kvcall, const Plan &P, uint64_t in_by
 }
 
 void launch_copy(Exec &E, const Launch &L, const Desc *dev_desc, const int64_t *dev_prefix, char *b0, char *b1,
-                 char *b2, const int32_t *live, hipStream_t s) {
-  // one workgroup per tile, or a fixed persistent grid
-  uint64_t cap = ATP_PERSIST ? uint64_t(E.grid_max) : (uint64_t(1) << 30);
+                 char *b2, const int32_t *live, hipStream_t s, uint64_t grid_cap = 0) {
+  // one workgroup per tile, or a fixed persistent grid (the kernels loop
+  // over the tiles of the launch)
+  uint64_t cap = grid_cap ? grid_cap : ATP_PERSIST ? uint64_t(E.grid_max) : (uint64_t(1) << 30);
   uint64_t g = std::min<uint64_t>(std::max<uint64_t>(L.tiles_max, 1), cap);
   if (L.aligned)
     hipLaunchKernelGGL(k_copy16, dim3(unsigned(g)), dim3(kThreads), 0, s, dev_desc, dev_prefix, L.d0, L.d1, b0, b1,
@@ -280,7 +401,8 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
                                 " bytes");
   if (kvcall && (!table || n_entries <= 0)) throw Error(ATP_EINVAL, "kv: block table missing");
   check_extents(c, kvcall, P, P.inplace ? arena_bytes : c.old_bytes, P.inplace ? arena_bytes : new_bytes,
-                staging_bytes);
+                staging_bytes, inflow_bytes, do_out ? outbound_bytes : 0);
+  if (!c.host_reads.empty()) check_kernel_host_buffer(inflow_host, inflow_bytes, "inflow buffer");
 
   int dev = -1;
   HIPCHK(hipGetDevice(&dev));
@@ -307,6 +429,10 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   int64_t *dev_prefix = reinterpret_cast<int64_t *>(b_st + c.off_prefix);
   int32_t *dev_err = reinterpret_cast<int32_t *>(b_st + c.off_meta);
   int32_t *dev_live = kvcall ? reinterpret_cast<int32_t *>(b_st + c.off_kvlive) : nullptr;
+
+  // the side streams are chosen before this call queues anything: the probe
+  // waits for what the caller's streams already hold
+  if (do_out) choose_side(E, compute, copy);
 
   // every stream starts after what the caller already queued on `compute`
   // The other call of a weights + KV pair may already be pending: its
@@ -353,55 +479,69 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   HIPCHK(hipGetLastError());
 
   // ---- outbound (in place): read before overwrite ---------------------------------
-  // issued in the plan's order (by the first level that overwrites them);
-  // pos_ev[k] fires when the first k + 1 of them have finished
-  std::vector<hipEvent_t> out_ev(c.outbound.size(), nullptr), pos_ev;
-  if (do_out && !kvcall) {
-    if (!E.d2h) E.d2h = E.stream();
-    HIPCHK(hipStreamWaitEvent(E.d2h, start, 0));
-    cs.d2h0 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.d2h0, E.d2h));
-    for (int o : c.out_order) {
-      const HostCopy &h = c.outbound[o];
-      if (h.rows <= 1)
-        HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_in + h.dev_off, h.bytes, hipMemcpyDeviceToHost, E.d2h));
-      else
-        HIPCHK(hipMemcpy2DAsync(host_out + h.host_off, h.run, b_in + h.dev_off, h.dev_pitch, h.run, h.rows,
-                                hipMemcpyDeviceToHost, E.d2h));
-      out_ev[o] = E.ev_sync();
-      HIPCHK(hipEventRecord(out_ev[o], E.d2h));
-      pos_ev.push_back(out_ev[o]);
-      cs.d2h_bytes += h.bytes;
-    }
-    cs.d2h1 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.d2h1, E.d2h));
-  }
-
-  // In place, the weight levels wait for outbound reads; that work and
-  // everything after it (ring landings, scatters, gated landings) runs on
-  // two library streams so that it does not hold up the caller's streams,
-  // and with them the other call's work.
+  // The weights call's outbound bytes are gathered by the copy kernel into a
+  // staging slot and leave with plain device-to-host copies, all on the side
+  // stream in the plan's order (by the first level that overwrites them);
+  // each level follows the gathers it needs, and pos_ev[k] fires once the
+  // first k + 1 outbound pieces are gathered.  That work and the weight
+  // inflow read after it stay off the caller's streams, so that they do not
+  // hold up the other call's work queued behind them.
+  std::vector<hipEvent_t> pos_ev;
   const bool split = do_out && !kvcall;
   hipStream_t late_copy = copy, late_comp = compute;
   if (split) {
-    if (!E.copy2) E.copy2 = E.stream();
-    if (!E.comp2) E.comp2 = E.stream();
-    late_copy = E.copy2;
-    late_comp = E.comp2;
-    hipEvent_t prepared = E.ev_sync();
+    late_comp = E.side;
+    hipEvent_t prepared = E.ev_sync();  // the gathers read the descriptors
     HIPCHK(hipEventRecord(prepared, compute));
     HIPCHK(hipStreamWaitEvent(late_comp, prepared, 0));
-    HIPCHK(hipStreamWaitEvent(late_copy, start, 0));
   }
+  std::vector<size_t> pos_of(c.outbound.size(), 0);
+  for (size_t p = 0; p < c.out_order.size(); ++p) pos_of[size_t(c.out_order[p])] = p;
+  size_t next_chunk = 0;
+  auto issue_outbound = [&](size_t upto) {  // gather at least the first `upto` pieces
+    while (pos_ev.size() < upto && next_chunk < c.out_chunks.size()) {
+      // in stream order a gather follows the copies out of the slot's last fill
+      const OutChunk &ch = c.out_chunks[next_chunk++];
+      for (const Launch &L : ch.gathers) {
+        CallState::LaunchRec r{3, -1, L.bytes, E.ev_time(), E.ev_time()};
+        HIPCHK(hipEventRecord(r.e0, late_comp));
+        launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
+        HIPCHK(hipEventRecord(r.e1, late_comp));
+        cs.launches.push_back(r);
+      }
+      if (size_t(ch.pos_end) > pos_ev.size()) {
+        hipEvent_t gathered = E.ev_sync();
+        HIPCHK(hipEventRecord(gathered, late_comp));
+        pos_ev.resize(size_t(ch.pos_end), gathered);
+      }
+      if (!cs.d2h0) {
+        cs.d2h0 = E.ev_time();
+        HIPCHK(hipEventRecord(cs.d2h0, late_comp));
+      }
+      for (const HostCopy &h : ch.d2h) {
+        HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_st + h.dev_off, h.bytes, hipMemcpyDeviceToHost, late_comp));
+        cs.d2h_bytes += h.bytes;
+      }
+    }
+  };
+  cs.d2h0 = cs.d2h1 = nullptr;
 
   // ---- repack levels ---------------------------------------------------------------
   std::vector<hipEvent_t> level_end(std::max(c.n_levels, 1), nullptr);
-  cs.rep0 = E.ev_time();
-  HIPCHK(hipEventRecord(cs.rep0, late_comp));
+  auto begin_levels = [&]() {
+    if (cs.rep0) return;
+    cs.rep0 = E.ev_time();
+    HIPCHK(hipEventRecord(cs.rep0, late_comp));
+  };
+  cs.rep0 = nullptr;
   for (size_t i = 0; i < c.levels.size(); ++i) {
     const Launch &L = c.levels[i];
-    for (int o : L.wait_outbound)
-      if (out_ev[o]) HIPCHK(hipStreamWaitEvent(late_comp, out_ev[o], 0));
+    if (split) {
+      size_t need = 0;
+      for (int o : L.wait_outbound) need = std::max(need, pos_of[size_t(o)] + 1);
+      issue_outbound(need);
+    }
+    begin_levels();
     CallState::LaunchRec r{kvcall ? 1 : 0, L.level, L.bytes, E.ev_time(), E.ev_time()};
     HIPCHK(hipEventRecord(r.e0, late_comp));
     launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
@@ -414,22 +554,42 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
       HIPCHK(hipEventRecord(level_end[L.level], late_comp));
     }
   }
+  if (split) {
+    issue_outbound(c.out_order.size());  // pieces no level waits for
+    if (cs.d2h0) {
+      cs.d2h1 = E.ev_time();
+      HIPCHK(hipEventRecord(cs.d2h1, late_comp));
+    }
+  }
+  begin_levels();
   cs.rep1 = E.ev_time();
   HIPCHK(hipEventRecord(cs.rep1, late_comp));  // also: prepare and every level are done
 
+  // in place: the copy kernel reads every gated or strided inflow piece from
+  // the pinned host buffer into its final place, after the last level (and,
+  // for the weights, after every outbound read)
+  for (const Launch &L : c.host_reads) {
+    CallState::LaunchRec r{4, -1, L.bytes, E.ev_time(), E.ev_time()};
+    HIPCHK(hipEventRecord(r.e0, late_comp));
+    launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, late_comp,
+                kHostReadGrid);
+    HIPCHK(hipEventRecord(r.e1, late_comp));
+    cs.launches.push_back(r);
+    cs.h2d_bytes += L.bytes;
+  }
+
   // KV outbound gathered into staging at level 0: copy it out after that level
   if (do_out && kvcall) {
-    if (!E.d2h) E.d2h = E.stream();
-    if (level_end[0]) HIPCHK(hipStreamWaitEvent(E.d2h, level_end[0], 0));
+    if (level_end[0]) HIPCHK(hipStreamWaitEvent(E.side, level_end[0], 0));
     cs.d2h0 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.d2h0, E.d2h));
+    HIPCHK(hipEventRecord(cs.d2h0, E.side));
     for (size_t o = 0; o < c.outbound.size(); ++o) {
       const HostCopy &h = c.outbound[o];
-      HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_st + h.dev_off, h.bytes, hipMemcpyDeviceToHost, E.d2h));
+      HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_st + h.dev_off, h.bytes, hipMemcpyDeviceToHost, E.side));
       cs.d2h_bytes += h.bytes;
     }
     cs.d2h1 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.d2h1, E.d2h));
+    HIPCHK(hipEventRecord(cs.d2h1, E.side));
   }
 
   // ---- inflow ------------------------------------------------------------------------
@@ -475,7 +635,15 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   for (const HostCopy &h : c.directs)
     if (h.gate_pos > 0) direct(h, late_copy);
   cs.h2d1 = E.ev_time();
-  HIPCHK(hipEventRecord(cs.h2d1, late_copy));
+  if (!c.host_reads.empty()) {
+    // the inflow ends with the later of the copy stream and the host reads
+    hipEvent_t copied = E.ev_sync();
+    HIPCHK(hipEventRecord(copied, late_copy));
+    HIPCHK(hipStreamWaitEvent(late_comp, copied, 0));
+    HIPCHK(hipEventRecord(cs.h2d1, late_comp));
+  } else {
+    HIPCHK(hipEventRecord(cs.h2d1, late_copy));
+  }
 
   // ---- tails ----------------------------------------------------------------------
   HIPCHK(hipMemcpyAsync(cs.err_host, dev_err, sizeof(int32_t), hipMemcpyDeviceToHost, compute));
@@ -486,7 +654,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   cs.tail_d2h = cs.tail_late_copy = cs.tail_late_comp = nullptr;
   if (do_out) {
     cs.tail_d2h = E.ev_sync();
-    HIPCHK(hipEventRecord(cs.tail_d2h, E.d2h));
+    HIPCHK(hipEventRecord(cs.tail_d2h, E.side));
   }
   if (split) {
     // the late streams are not joined back into the caller's streams (that
@@ -514,6 +682,7 @@ int exec_sync(Plan &P, atp_timing *out) {
   };
   double h2d_ms = 0, rep_ms = 0;
   hipEvent_t h2d_first = nullptr, h2d_last = nullptr;  // union span of both calls
+  const bool was_pending[2] = {E.w.pending, E.k.pending};
   for (int which = 0; which < 2; ++which) {
     CallState &cs = which == 0 ? E.w : E.k;
     if (!cs.pending) continue;
@@ -535,12 +704,13 @@ int exec_sync(Plan &P, atp_timing *out) {
     // busy time of the repack kernels (levels), and the span they cover
     double busy = 0;
     for (const auto &L : cs.launches)
-      if (L.kind != 2) busy += ms(L.e0, L.e1);
+      if (L.kind < 2) busy += ms(L.e0, L.e1);
     (which == 0 ? t.repack_w_ms : t.repack_kv_ms) = busy;
     t.repack_span_ms += ms(cs.rep0, cs.rep1);
     rep_ms += busy;
-    h2d_first = h2d_first ? h2d_first : cs.h2d0;
-    if (cs.h2d1) h2d_last = cs.h2d1;
+    // union span of both calls: the earlier start, the later end
+    if (cs.h2d0 && (!h2d_first || ms(cs.h2d0, h2d_first) > 0)) h2d_first = cs.h2d0;
+    if (cs.h2d1 && (!h2d_last || ms(h2d_last, cs.h2d1) > 0)) h2d_last = cs.h2d1;
     t.d2h_ms = std::max(t.d2h_ms, ms(cs.d2h0, cs.d2h1));
     for (const auto &L : cs.launches) {
       double m = ms(L.e0, L.e1);
@@ -554,6 +724,29 @@ int exec_sync(Plan &P, atp_timing *out) {
   }
   h2d_ms = ms(h2d_first, h2d_last);
   t.h2d_ms = h2d_ms;
+  // union of the repack kernels' intervals over both calls, on a common
+  // time origin (the start of the inflow)
+  if (h2d_first) {
+    std::vector<std::pair<double, double>> iv;
+    for (int which = 0; which < 2; ++which)
+      if (was_pending[which])
+        for (const auto &L : (which == 0 ? E.w : E.k).launches)
+          if (L.kind < 2 && L.e0 && L.e1) iv.push_back({ms(h2d_first, L.e0), ms(h2d_first, L.e1)});
+    std::sort(iv.begin(), iv.end());
+    double cur_lo = 0, cur_hi = 0;
+    bool open = false;
+    for (const auto &x : iv) {
+      if (open && x.first <= cur_hi) {
+        cur_hi = std::max(cur_hi, x.second);
+        continue;
+      }
+      if (open) t.repack_union_ms += cur_hi - cur_lo;
+      cur_lo = x.first;
+      cur_hi = x.second;
+      open = true;
+    }
+    if (open) t.repack_union_ms += cur_hi - cur_lo;
+  }
   t.wall_ms = E.wall_started
                   ? std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - E.wall0).count()
                   : 0;

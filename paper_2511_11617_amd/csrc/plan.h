@@ -57,7 +57,7 @@ struct TensorPlan {
 // One kernel launch over a contiguous descriptor range.
 struct Launch {
   int level = 0;
-  int kind = 0;        // 0 repack, 2 scatter
+  int kind = 0;        // 0 repack, 2 scatter, 3 outbound gather, 4 host read
   bool aligned = true;
   int d0 = 0, d1 = 0;
   uint64_t bytes = 0;  // bytes copied (upper bound for block ranges)
@@ -86,6 +86,14 @@ struct Chunk {
   std::vector<Launch> scatters;   // aligned and/or 2-byte-granular
 };
 
+// Outbound slot fill: gathers into the slot, then its device-to-host copies.
+struct OutChunk {
+  int slot = 0;
+  std::vector<Launch> gathers;   // arena -> staging slot
+  std::vector<HostCopy> d2h;     // staging slot -> host, one per piece
+  int pos_end = 0;               // positions of out_order complete after it
+};
+
 // Everything one reshard call (weights or KV) executes.
 struct CallPlan {
   std::vector<Fam> fams;        // final families, index = descriptor index
@@ -94,6 +102,19 @@ struct CallPlan {
   std::vector<Chunk> chunks;
   std::vector<HostCopy> outbound;
   std::vector<int> out_order;   // outbound issue order (by the level needing it)
+  // In place, no host-to-device copy command waits long for an event: such
+  // a command holds up every later host-to-device copy of the process on
+  // the DMA engine.  Every weight inflow piece that waits for a level or an
+  // outbound read is read by the copy kernel straight from the pinned
+  // inflow buffer after the call's last level (KV inflow takes the landing
+  // ring, which waits only for its own scatters).  The weights' outbound reads are gathered by the copy kernel into
+  // a staging slot in out_order, then leave with plain device-to-host
+  // copies; a level waits only for the gathers of what it overwrites (and,
+  // in stream order, for the copies out of the slot before them).
+  std::vector<Launch> host_reads;
+  std::vector<OutChunk> out_chunks;
+  uint64_t off_oslot = 0, oslot = 0;
+  int n_oslots = 0;
   std::vector<atp_segment> seg_in, seg_out;
   int n_levels = 0;
   uint64_t retained = 0, moved = 0, staged = 0;

@@ -80,8 +80,11 @@ def test_bad_gqa_reference_is_einval():
 
 def test_in_place_staging_cap_too_small_is_ecapacity():
     c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=256)
-    with pytest.raises(atp.AtpError) as e:
-        _plan(c, flags=atp.INPLACE, staging_cap=1 << 16)
+    st = _plan(c, flags=atp.INPLACE, staging_cap=1 << 30).stats()
+    need = max(st.staging_w, st.staging_kv)
+    _plan(c, flags=atp.INPLACE, staging_cap=need)  # exactly enough
+    with pytest.raises(atp.AtpError) as e:  # less than the descriptors alone
+        _plan(c, flags=atp.INPLACE, staging_cap=1 << 12)
     assert e.value.code == atp.ECAPACITY
 
 
