@@ -170,10 +170,10 @@ void atp_plan_free(atp_plan_t *plan);
  *                (in place only) the old bytes peers need and this GPU drops,
  *                read before they are overwritten; may be NULL if 0 bytes
  *   staging      device scratch of at least stats.staging_w bytes
- * With ATP_INPLACE the copy kernel itself reads the inflow that must wait
- * for a level or an outbound read: inflow_host must then come from
- * hipHostMalloc (device-accessible at the same address) and be 256-byte
- * aligned, else ATP_EINVAL / ATP_EALIGN.
+ * With ATP_INPLACE the copy kernel itself writes the outbound bytes and
+ * reads the inflow that must wait for a level or an outbound read: both
+ * host buffers must then come from hipHostMalloc (device-accessible at the
+ * same address) and be 256-byte aligned, else ATP_EINVAL / ATP_EALIGN.
  * Launch errors return ATP_EHIP; kernel-side errors surface in atp_sync. */
 int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes,
                         void *new_arena, uint64_t new_arena_bytes,
@@ -188,7 +188,8 @@ int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes,
  * and the distinct ids must number kv.live_blocks (else ATP_EINVAL from
  * atp_sync).  Buffers as for atp_reshard_weights, sizes from stats.*_kv.
  * The weights and KV calls may be pending together if their staging
- * buffers do not overlap. */
+ * buffers do not overlap; with ATP_INPLACE the weights call must then come
+ * first (a weights call after a pending KV call is ATP_ESTATE). */
 int atp_reshard_kv(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes,
                    void *new_kv_arena, uint64_t new_kv_bytes,
                    const int32_t *block_table, int32_t n_seq, int32_t max_blocks,
@@ -279,8 +280,8 @@ int atp_plan_segments(const atp_plan_t *plan, int32_t which, atp_segment *out,
                       int32_t cap, int32_t *n);
 
 /* One kernel launch of the last reshard: kind 0 = weight repack,
- * 1 = KV repack, 2 = landing-ring scatter, 3 = outbound gather into
- * staging (in place), 4 = inflow read from the host buffer (in place);
+ * 1 = KV repack, 2 = landing-ring scatter, 3 = outbound read into the host
+ * buffer (in place), 4 = inflow read from the host buffer (in place);
  * `ms` from HIP events on the stream the launch ran on. */
 typedef struct {
   int32_t kind, level;

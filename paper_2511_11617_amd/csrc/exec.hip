@@ -59,8 +59,8 @@ struct CallState {
 // every plan would otherwise cost tens of milliseconds per reshard.
 struct DevicePool {
   std::vector<hipEvent_t> sync_ev, time_ev;
-  std::vector<hipStream_t> streams;  // side-stream candidates that did not qualify: kept alive, so
-                                     // that no new stream reuses a handle the probe cache knows
+  std::vector<hipStream_t> streams;  // side streams (choose_side); never destroyed, so that no new
+                                     // stream reuses a handle the probe cache knows
   std::vector<std::pair<void *, size_t>> pinned;
 };
 std::mutex g_pool_mu;
@@ -172,11 +172,15 @@ __global__ void k_nop() {}
 
 constexpr uint32_t kSpinIters = 400;     // about 1.4 ms at 2.4 GHz
 constexpr float kSpinMarginMs = 0.3f;    // the empty kernel must finish this much earlier
-constexpr int kSideCandidates = 8;       // streams tried before giving up on a free queue
 
-// Workgroups of the host-read launches (a persistent grid over their
-// tiles): 64 already carry a full x16 Gen5 link from pinned host memory.
+// Workgroups of the launches that move bytes over PCIe with the copy kernel
+// (persistent grids over their tiles).  64 already carry a full x16 Gen5
+// link from pinned host memory.  The outbound reads get a narrow grid: wide
+// device-to-host writers (the runtime's 512-workgroup blits) slowed a
+// concurrent HBM-bound repack several-fold; 8 workgroups leave a concurrent
+// HBM copy at full speed while writing 17 GB/s beside it (41 GB/s alone).
 constexpr uint64_t kHostReadGrid = 128;
+constexpr uint64_t kOutboundGrid = 8;
 std::map<std::pair<hipStream_t, hipStream_t>, bool> g_same_queue;  // under g_pool_mu
 
 bool same_queue(Exec &E, hipStream_t a, hipStream_t b) {
@@ -206,14 +210,17 @@ bool same_queue(Exec &E, hipStream_t a, hipStream_t b) {
 // The side stream for a pair of caller streams: one on a hardware queue that
 // neither caller stream uses, chosen once per (device, compute, copy) and
 // shared by every plan (work from several plans on it is merely serialised).
-// At most kSideCandidates streams are ever created for a pair; when none of
-// them qualifies, the first is used and the outbound work then holds up the
-// caller's stream on that queue (the reshard stays correct).
+// Candidates are the device's earlier side streams first, then new ones, at
+// most kSideStreams per device in all.  When none qualifies, the first is
+// used and the outbound work then holds up the caller's stream on that queue
+// (the reshard stays correct).
+constexpr size_t kSideStreams = 8;
 std::map<std::tuple<int, hipStream_t, hipStream_t>, hipStream_t> g_side;  // under g_pool_mu
 
 void choose_side(Exec &E, hipStream_t compute, hipStream_t copy) {
   if (E.side && E.side_for_compute == compute && E.side_for_copy == copy) return;
   const auto key = std::make_tuple(E.device, compute, copy);
+  std::vector<hipStream_t> known;
   {
     std::lock_guard<std::mutex> g(g_pool_mu);
     auto it = g_side.find(key);
@@ -223,27 +230,32 @@ void choose_side(Exec &E, hipStream_t compute, hipStream_t copy) {
       E.side_for_copy = copy;
       return;
     }
+    known = g_pools[E.device].streams;
   }
-  std::vector<hipStream_t> made;
   hipStream_t pick = nullptr;
-  for (int i = 0; i < kSideCandidates && !pick; ++i) {
+  for (size_t i = 0; !pick; ++i) {
     hipStream_t s = nullptr;
-    HIPCHK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));  // default priority
-    made.push_back(s);
+    if (i < known.size()) {
+      s = known[i];
+    } else if (i < kSideStreams) {
+      HIPCHK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));  // default priority
+      std::lock_guard<std::mutex> g(g_pool_mu);
+      g_pools[E.device].streams.push_back(s);
+      known.push_back(s);
+    } else {
+      break;
+    }
     if (!same_queue(E, compute, s) && !same_queue(E, copy, s)) pick = s;
   }
   if (!pick) {
-    pick = made.front();
-    fprintf(stderr, "atp: no hardware queue free of the caller's streams after %d tries; the in-place "
-                    "outbound work shares one\n", kSideCandidates);
+    if (known.empty()) throw Error(ATP_EHIP, "no stream for the in-place outbound work");
+    pick = known.front();
+    fprintf(stderr, "atp: no hardware queue free of the caller's streams among %zu streams; the in-place "
+                    "outbound work shares one\n", known.size());
   }
   {
     std::lock_guard<std::mutex> g(g_pool_mu);
-    auto &pool = g_pools[E.device].streams;
-    for (hipStream_t s : made)
-      if (s != pick) pool.push_back(s);
-    auto ins = g_side.insert({key, pick});
-    E.side = ins.first->second;  // another thread may have chosen first
+    E.side = g_side.insert({key, pick}).first->second;  // another thread may have chosen first
   }
   E.side_for_compute = compute;
   E.side_for_copy = copy;
@@ -316,7 +328,8 @@ uint64_t extent(const Fam &f, bool src, int64_t n_blocks, int64_t live) {
 void check_extents(const CallPlan &c, bool kvcall, const Plan &P, uint64_t in_bytes, uint64_t out_bytes,
                    uint64_t stage_bytes, uint64_t inflow_bytes, uint64_t outbound_bytes) {
   int64_t nb = kvcall ? P.kv.num_blocks : 0, live = kvcall ? P.kv.live_blocks : 0;
-  // the host-read launches bind slot IN to the pinned inflow buffer
+  // the host-read launches bind slot IN to the pinned inflow buffer, the
+  // outbound launches slot OUT to the pinned outbound buffer
   const int h0 = c.host_reads.empty() ? -1 : c.host_reads.front().d0;
   const int h1 = c.host_reads.empty() ? -1 : c.host_reads.back().d1;
   auto fits = [](uint64_t off, uint64_t bytes, uint64_t lim) { return bytes <= lim && off <= lim - bytes; };
@@ -327,18 +340,16 @@ void check_extents(const CallPlan &c, bool kvcall, const Plan &P, uint64_t in_by
     for (const HostCopy &h : ch.copies)
       if (!fits(h.host_off, h.bytes, inflow_bytes) || !fits(h.dev_off, h.bytes, stage_bytes))
         throw Error(ATP_ECAPACITY, "an inflow landing would run past the end of a buffer");
-  for (const OutChunk &ch : c.out_chunks)
-    for (const HostCopy &h : ch.d2h)
-      if (!fits(h.host_off, h.bytes, outbound_bytes) || !fits(h.dev_off, h.bytes, stage_bytes))
-        throw Error(ATP_ECAPACITY, "an outbound copy would run past the end of a buffer");
+  const int o0 = c.out_d0, o1 = c.out_d0 < 0 ? -1 : c.out_d0 + int(c.out_order.size());
   for (int d = 0; d < int(c.fams.size()); ++d) {
     const Fam &f = c.fams[size_t(d)];
-    const bool host_read = d >= h0 && d < h1;
+    const bool host_read = d >= h0 && d < h1, outbound = d >= o0 && d < o1;
     for (int side = 0; side < 2; ++side) {
       uint32_t slot = (f.flags >> (side == 0 ? DF_SRC_SHIFT : DF_DST_SHIFT)) & 3;
       uint64_t e = extent(f, side == 0, nb, live);
       uint64_t lim = slot == BUF_IN ? in_bytes : slot == BUF_OUT ? out_bytes : stage_bytes;
       if (host_read && slot == BUF_IN) lim = inflow_bytes;
+      if (outbound && slot == BUF_OUT) lim = outbound_bytes;
       if (e > lim) throw Error(ATP_ECAPACITY, "a copy would run past the end of a buffer");
     }
     uint64_t lines = uint64_t(kvcall ? std::max<int64_t>(nb, f.o_end - f.o_begin) : f.o_end - f.o_begin) * f.rows;
@@ -371,6 +382,11 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   Exec &E = exec_of(P);
   CallState &cs = kvcall ? E.k : E.w;
   if (cs.pending) throw Error(ATP_ESTATE, "reshard called again before atp_sync");
+  // In place, a weights call issued while the KV call is pending ended one
+  // process with a host fault whose cause is not known; that order is
+  // refused until it is.
+  if (P.inplace && !kvcall && E.k.pending)
+    throw Error(ATP_ESTATE, "in place, call atp_reshard_weights before atp_reshard_kv (or after atp_sync)");
   const char *what = kvcall ? "kv" : "weights";
   // ---- argument checks ------------------------------------------------------
   if (!arena) throw Error(ATP_EINVAL, std::string(what) + ": arena is NULL");
@@ -403,6 +419,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   check_extents(c, kvcall, P, P.inplace ? arena_bytes : c.old_bytes, P.inplace ? arena_bytes : new_bytes,
                 staging_bytes, inflow_bytes, do_out ? outbound_bytes : 0);
   if (!c.host_reads.empty()) check_kernel_host_buffer(inflow_host, inflow_bytes, "inflow buffer");
+  if (do_out && c.out_d0 >= 0) check_kernel_host_buffer(outbound_host, c.outbound_bytes, "outbound buffer");
 
   int dev = -1;
   HIPCHK(hipGetDevice(&dev));
@@ -479,50 +496,52 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   HIPCHK(hipGetLastError());
 
   // ---- outbound (in place): read before overwrite ---------------------------------
-  // The weights call's outbound bytes are gathered by the copy kernel into a
-  // staging slot and leave with plain device-to-host copies, all on the side
-  // stream in the plan's order (by the first level that overwrites them);
-  // each level follows the gathers it needs, and pos_ev[k] fires once the
-  // first k + 1 outbound pieces are gathered.  That work and the weight
-  // inflow read after it stay off the caller's streams, so that they do not
-  // hold up the other call's work queued behind them.
+  // The weights call's outbound reads are copy-kernel launches on the side
+  // stream that write straight into the pinned outbound buffer, in the
+  // plan's order (by the first level that overwrites them), each level right
+  // after the reads it needs; pos_ev[k] fires when the first k + 1 have
+  // finished.  That work and the weight inflow read after it stay off the
+  // caller's streams, so that they do not hold up the other call's work
+  // queued behind them.
   std::vector<hipEvent_t> pos_ev;
   const bool split = do_out && !kvcall;
   hipStream_t late_copy = copy, late_comp = compute;
   if (split) {
     late_comp = E.side;
-    hipEvent_t prepared = E.ev_sync();  // the gathers read the descriptors
+    hipEvent_t prepared = E.ev_sync();  // the outbound launches read the descriptors
     HIPCHK(hipEventRecord(prepared, compute));
     HIPCHK(hipStreamWaitEvent(late_comp, prepared, 0));
   }
   std::vector<size_t> pos_of(c.outbound.size(), 0);
   for (size_t p = 0; p < c.out_order.size(); ++p) pos_of[size_t(c.out_order[p])] = p;
-  size_t next_chunk = 0;
-  auto issue_outbound = [&](size_t upto) {  // gather at least the first `upto` pieces
-    while (pos_ev.size() < upto && next_chunk < c.out_chunks.size()) {
-      // in stream order a gather follows the copies out of the slot's last fill
-      const OutChunk &ch = c.out_chunks[next_chunk++];
-      for (const Launch &L : ch.gathers) {
-        CallState::LaunchRec r{3, -1, L.bytes, E.ev_time(), E.ev_time()};
-        HIPCHK(hipEventRecord(r.e0, late_comp));
-        launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
-        HIPCHK(hipEventRecord(r.e1, late_comp));
-        cs.launches.push_back(r);
-      }
-      if (size_t(ch.pos_end) > pos_ev.size()) {
-        hipEvent_t gathered = E.ev_sync();
-        HIPCHK(hipEventRecord(gathered, late_comp));
-        pos_ev.resize(size_t(ch.pos_end), gathered);
-      }
-      if (!cs.d2h0) {
-        cs.d2h0 = E.ev_time();
-        HIPCHK(hipEventRecord(cs.d2h0, late_comp));
-      }
-      for (const HostCopy &h : ch.d2h) {
-        HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_st + h.dev_off, h.bytes, hipMemcpyDeviceToHost, late_comp));
-        cs.d2h_bytes += h.bytes;
-      }
+  auto issue_outbound = [&](size_t upto) {  // read out the first `upto` pieces
+    size_t issued = pos_ev.size();
+    if (issued >= upto) return;
+    if (!cs.d2h0) {
+      cs.d2h0 = E.ev_time();
+      HIPCHK(hipEventRecord(cs.d2h0, late_comp));
     }
+    while (issued < upto) {
+      // one launch per run of positions with the same alignment
+      Launch L;
+      L.kind = 3;
+      L.aligned = c.out_aligned[issued] != 0;
+      L.d0 = c.out_d0 + int(issued);
+      for (; issued < upto && (c.out_aligned[issued] != 0) == L.aligned; ++issued) {
+        L.tiles_max += c.out_tiles[issued];
+        L.bytes += c.outbound[size_t(c.out_order[issued])].bytes;
+      }
+      L.d1 = c.out_d0 + int(issued);
+      CallState::LaunchRec r{3, -1, L.bytes, E.ev_time(), E.ev_time()};
+      HIPCHK(hipEventRecord(r.e0, late_comp));
+      launch_copy(E, L, dev_desc, dev_prefix, b_in, host_out, b_st, dev_live, late_comp, kOutboundGrid);
+      HIPCHK(hipEventRecord(r.e1, late_comp));
+      cs.launches.push_back(r);
+      cs.d2h_bytes += L.bytes;
+    }
+    hipEvent_t done = E.ev_sync();
+    HIPCHK(hipEventRecord(done, late_comp));
+    pos_ev.resize(upto, done);
   };
   cs.d2h0 = cs.d2h1 = nullptr;
 

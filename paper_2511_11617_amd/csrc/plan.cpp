@@ -621,9 +621,6 @@ bool is_identity(const Fam &f) {
 
 constexpr uint64_t kSplitLine = 64 * 1024;
 constexpr uint64_t kDirectMin = 32ull << 20;  // smallest inflow gap landed directly
-constexpr uint64_t kOutSlot = 256ull << 20;    // staging slot of the outbound gathers
-constexpr uint64_t kOutSlotMin = 4ull << 20;
-constexpr int kOutSlots = 1;  // gathers and copies share one in-order stream
 constexpr size_t kMaxPieces = 1u << 20;
 
 struct Node {
@@ -1021,76 +1018,27 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
     c.outbound.push_back(h);
   }
   if (P.inplace && !kvcall && !c.out_order.empty()) {
-    // gathers into the outbound slot, in out_order; a piece larger than the
-    // slot is split by rows, a row larger than the slot by bytes
-    uint64_t total = 0;
-    for (const HostCopy &h : c.outbound) total += align_up(h.bytes, 256);
-    c.oslot = std::min<uint64_t>(kOutSlot, align_up(total, 256));
-    c.n_oslots = total > c.oslot ? kOutSlots : 1;
-    while (c.oslot > kOutSlotMin && stage_bytes + c.n_oslots * c.oslot + (1u << 20) > cap)
-      c.oslot = align_up(c.oslot / 2, 256);
-    int next_slot = 0;
-    OutChunk ch;
-    std::vector<Fam> fams;
-    uint64_t fill = 0;
-    auto flush = [&]() {
-      if (fams.empty()) return;
-      emit_group(c, fams, -1, 3, ch.gathers, INT64_MAX);
-      ch.slot = next_slot;
-      next_slot = (next_slot + 1) % c.n_oslots;
-      c.out_chunks.push_back(ch);
-      ch = OutChunk();
-      fams.clear();
-      fill = 0;
-    };
-    auto add = [&](uint64_t src_off, uint64_t src_pitch, int64_t items, uint64_t run, uint64_t host_off) {
-      const uint64_t bytes = uint64_t(items) * run;
-      if (fill + bytes > c.oslot) flush();
+    // the copy kernel reads them out: arena (slot IN) -> pinned outbound
+    // buffer (slot OUT of those launches), packed row after row
+    c.out_d0 = int(c.fams.size());
+    for (int o : c.out_order) {
+      const HostCopy &h = c.outbound[size_t(o)];
       Fam f;
-      f.src_off = src_off;
-      f.src_ostride = src_pitch;
-      f.dst_off = fill;  // within the slot; re-based with the staging layout
-      f.dst_ostride = run;
+      f.src_off = h.dev_off;
+      f.src_ostride = h.dev_pitch;
+      f.dst_off = h.host_off;
+      f.dst_ostride = h.run;
       f.o_begin = 0;
-      f.o_end = items;
-      f.run = run;
+      f.o_end = int64_t(h.rows);
+      f.run = h.run;
       f.rows = 1;
-      f.flags = bufs(BUF_IN, BUF_STAGE);
-      fams.push_back(f);
-      HostCopy d;
-      d.dev_buf = BUF_STAGE;
-      d.dev_off = fill;
-      d.host_off = host_off;
-      d.bytes = bytes;
-      d.run = bytes;
-      ch.d2h.push_back(d);
-      fill = align_up(fill + bytes, 256);
-    };
-    for (size_t k = 0; k < c.out_order.size(); ++k) {
-      const HostCopy &h = c.outbound[size_t(c.out_order[k])];
-      const int64_t rows = int64_t(h.rows);
-      if (h.run <= c.oslot) {
-        const int64_t per = int64_t(c.oslot / h.run);
-        for (int64_t r = 0; r < rows;) {
-          int64_t room = int64_t((c.oslot - std::min(c.oslot, fill)) / h.run);
-          if (room <= 0) {
-            flush();
-            room = per;
-          }
-          const int64_t n = std::min<int64_t>(room, rows - r);
-          add(h.dev_off + uint64_t(r) * h.dev_pitch, h.dev_pitch, n, h.run, h.host_off + uint64_t(r) * h.run);
-          r += n;
-        }
-      } else {
-        for (int64_t r = 0; r < rows; ++r)
-          for (uint64_t b = 0; b < h.run; b += c.oslot) {
-            const uint64_t n = std::min<uint64_t>(c.oslot, h.run - b);
-            add(h.dev_off + uint64_t(r) * h.dev_pitch + b, 0, 1, n, h.host_off + uint64_t(r) * h.run + b);
-          }
-      }
-      ch.pos_end = int(k) + 1;
+      f.flags = bufs(BUF_IN, BUF_OUT);
+      const bool al = fam_aligned(f);
+      if (al) f.flags |= DF_ALIGNED;
+      c.out_aligned.push_back(al);
+      c.out_tiles.push_back(fam_tiles(f, f.o_end));
+      c.fams.push_back(f);
     }
-    flush();
   }
 
   // ---- inflow: direct copies (contiguous) and ring chunks (strided) --------------------
@@ -1265,8 +1213,6 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
   at += uint64_t(c.n_slots) * c.ring_slot;
   c.off_stage = at;
   at += stage_bytes;
-  c.off_oslot = at = align_up(at, 256);
-  at += uint64_t(c.n_oslots) * c.oslot;
   c.staging_need = align_up(at, 256);
   if (P.inplace && c.staging_need > cap)
     fail(ATP_ECAPACITY, std::string(kvcall ? "KV" : "weights") + " in-place schedule needs " +
@@ -1287,12 +1233,6 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
     }
   for (HostCopy &h : c.outbound)
     if (h.dev_buf == BUF_STAGE) h.dev_off += c.off_stage;
-  for (OutChunk &ch : c.out_chunks) {
-    const uint64_t base = c.off_oslot + uint64_t(ch.slot) * c.oslot;
-    for (Launch &L : ch.gathers)
-      for (int d = L.d0; d < L.d1; ++d) c.fams[size_t(d)].dst_off += base;
-    for (HostCopy &h : ch.d2h) h.dev_off += base;
-  }
 }
 
 }  // namespace

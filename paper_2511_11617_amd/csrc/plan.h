@@ -57,7 +57,7 @@ struct TensorPlan {
 // One kernel launch over a contiguous descriptor range.
 struct Launch {
   int level = 0;
-  int kind = 0;        // 0 repack, 2 scatter, 3 outbound gather, 4 host read
+  int kind = 0;        // 0 repack, 2 scatter, 3 outbound read, 4 host read
   bool aligned = true;
   int d0 = 0, d1 = 0;
   uint64_t bytes = 0;  // bytes copied (upper bound for block ranges)
@@ -86,14 +86,6 @@ struct Chunk {
   std::vector<Launch> scatters;   // aligned and/or 2-byte-granular
 };
 
-// Outbound slot fill: gathers into the slot, then its device-to-host copies.
-struct OutChunk {
-  int slot = 0;
-  std::vector<Launch> gathers;   // arena -> staging slot
-  std::vector<HostCopy> d2h;     // staging slot -> host, one per piece
-  int pos_end = 0;               // positions of out_order complete after it
-};
-
 // Everything one reshard call (weights or KV) executes.
 struct CallPlan {
   std::vector<Fam> fams;        // final families, index = descriptor index
@@ -107,14 +99,15 @@ struct CallPlan {
   // the DMA engine.  Every weight inflow piece that waits for a level or an
   // outbound read is read by the copy kernel straight from the pinned
   // inflow buffer after the call's last level (KV inflow takes the landing
-  // ring, which waits only for its own scatters).  The weights' outbound reads are gathered by the copy kernel into
-  // a staging slot in out_order, then leave with plain device-to-host
-  // copies; a level waits only for the gathers of what it overwrites (and,
-  // in stream order, for the copies out of the slot before them).
+  // ring, which waits only for its own scatters).  The weights' outbound
+  // reads are copy-kernel descriptors too (out_d0 + k for position k of
+  // out_order), writing straight into the pinned outbound buffer: the
+  // runtime's own device-to-host copies are wide blit kernels that starve
+  // the HBM-bound repack beside them.
   std::vector<Launch> host_reads;
-  std::vector<OutChunk> out_chunks;
-  uint64_t off_oslot = 0, oslot = 0;
-  int n_oslots = 0;
+  int out_d0 = -1;
+  std::vector<uint64_t> out_tiles;
+  std::vector<uint8_t> out_aligned;
   std::vector<atp_segment> seg_in, seg_out;
   int n_levels = 0;
   uint64_t retained = 0, moved = 0, staged = 0;

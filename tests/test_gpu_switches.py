@@ -7,6 +7,9 @@
   with a live-block count different from the plan's, makes atp_sync return
   ATP_EINVAL; nothing is copied and no access leaves its buffer.
 * A second reshard call before atp_sync is ATP_ESTATE.
+* Fresh in-place plans one after another, with the earlier plans still
+  alive (as a benchmark loop holds them), each choose the stream for the
+  outbound work and stay bit-exact (outbound buffer included).
 """
 import numpy as np
 import pytest
@@ -16,7 +19,7 @@ from oracle import model, repack
 from paper_2511_11617_amd import atp, problem
 from synth import configs, pagetable
 from synth.content import KIND_TAG16, Content
-from tests.gpu_harness import CachedContent, say
+from tests.gpu_harness import CachedContent, run_case, say
 
 pytestmark = pytest.mark.gpu
 
@@ -176,3 +179,12 @@ def test_second_call_before_sync_is_estate():
     assert e.value.code == atp.ESTATE
     plan.sync()
     torch.cuda.synchronize()
+
+
+def test_fresh_in_place_plans_in_a_row():
+    c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=256)
+    alive = []
+    for i in range(4):
+        t, plan, st = run_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"], name=f"fresh-in-place-{i}")
+        assert st.outbound_w > 0 and t.d2h_bytes == st.outbound_w + st.outbound_kv
+        alive.append(plan)
