@@ -410,6 +410,58 @@ int atp_kv_evict_lru(const int32_t *table, int32_t n_seq, int32_t max_blocks, in
                      const int64_t *last_use, uint64_t block_bytes, uint64_t budget_bytes,
                      int32_t compact, int32_t *keep, int32_t *new_table, atp_evict_stats *stats);
 
+/* ---- state plane (Sec. III-A: a daemon, decoupled from the inference
+ * process, keeps the GPU memory of the weights and the KV cache; inference
+ * processes obtain handles to it over IPC and read and write it, so the
+ * state survives a crashed inference process and a new one resumes on it;
+ * the state plane also keeps each session's recency for the KV budget) ---- */
+typedef struct atp_state_obj atp_state_t;
+
+/* Run the daemon in the calling thread: listen on the Unix socket
+ * `socket_path` (a stale socket file is replaced; a path another daemon
+ * answers on is ATP_EINVAL), serve requests until atp_state_shutdown, then
+ * free every region it holds and return ATP_OK.  The daemon owns each
+ * region it allocates on `device` (hipMalloc + hipIpcGetMemHandle); it
+ * touches the device only at the first allocation.  Regions are limited to
+ * 2 GiB - 1 MiB each: larger IPC allocations have not opened reliably on
+ * this platform. */
+int atp_daemon_serve(const char *socket_path, int32_t device);
+
+/* Connect to the daemon at `socket_path` (ATP_EINVAL if none answers).  One
+ * connection belongs to one thread at a time.  atp_state_disconnect unmaps
+ * every region the connection opened and closes it; the regions stay with
+ * the daemon (as they do when the process dies). */
+int atp_state_connect(const char *socket_path, atp_state_t **out);
+void atp_state_disconnect(atp_state_t *state);
+
+/* Ask the daemon for a new device region of `bytes` named `name` and map it
+ * into this process at *dev_ptr (256-byte aligned, contents undefined).
+ * ATP_EINVAL for an existing name or a size outside [1, 2 GiB - 1 MiB];
+ * ATP_EHIP when the daemon or this process cannot allocate or map it. */
+int atp_state_alloc(atp_state_t *state, const char *name, uint64_t bytes, void **dev_ptr);
+/* Map the existing region `name`; *bytes (nullable) receives its size. */
+int atp_state_open(atp_state_t *state, const char *name, void **dev_ptr, uint64_t *bytes);
+/* Unmap a region this connection mapped (the daemon keeps it). */
+int atp_state_release(atp_state_t *state, void *dev_ptr);
+/* Unmap (here) and free (in the daemon) the region `name`. */
+int atp_state_free(atp_state_t *state, const char *name);
+
+/* Named host blobs kept by the daemon (block tables, per-session last use):
+ * put replaces, get copies out.  atp_state_get with data = NULL only
+ * reports the size in *bytes; a `cap` below the size is ATP_ECAPACITY with
+ * *bytes set.  A missing name is ATP_EINVAL.  Blobs are at most 4 GiB. */
+int atp_state_put(atp_state_t *state, const char *name, const void *data, uint64_t bytes);
+int atp_state_get(atp_state_t *state, const char *name, void *data, uint64_t cap, uint64_t *bytes);
+
+/* Text listing ("region <name> <bytes>" / "blob <name> <bytes>" lines,
+ * NUL-terminated) of what the daemon holds; *bytes receives the size with
+ * the terminator, text may be NULL to ask for it. */
+int atp_state_list(atp_state_t *state, char *text, uint64_t cap, uint64_t *bytes);
+
+/* Ask the daemon to free everything and stop.  A lost connection to the
+ * daemon is ATP_ESTATE for every call. */
+int atp_state_shutdown(atp_state_t *state);
+
 const char *atp_last_error(void);
 
 #ifdef __cplusplus

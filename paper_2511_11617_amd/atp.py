@@ -35,7 +35,9 @@ EXPORTS = [
     "atp_plan_stats", "atp_plan_tasks", "atp_plan_ranges", "atp_plan_owner",
     "atp_plan_layout", "atp_plan_segments", "atp_plan_launches", "atp_partition",
     "atp_last_error", "atp_st_open", "atp_st_close", "atp_st_find", "atp_load_weights",
-    "atp_kv_evict_lru",
+    "atp_kv_evict_lru", "atp_daemon_serve", "atp_state_connect", "atp_state_disconnect",
+    "atp_state_alloc", "atp_state_open", "atp_state_release", "atp_state_free", "atp_state_put",
+    "atp_state_get", "atp_state_list", "atp_state_shutdown",
 ]
 
 
@@ -169,9 +171,21 @@ def _load():
                                      C.POINTER(LoadStats)]
     lib.atp_kv_evict_lru.argtypes = [P, C.c_int32, C.c_int32, C.c_int64, P, C.c_uint64, C.c_uint64, C.c_int32,
                                      P, P, C.POINTER(EvictStats)]
+    lib.atp_daemon_serve.argtypes = [C.c_char_p, C.c_int32]
+    lib.atp_state_connect.argtypes = [C.c_char_p, C.POINTER(P)]
+    lib.atp_state_disconnect.argtypes = [P]
+    lib.atp_state_disconnect.restype = None
+    lib.atp_state_alloc.argtypes = [P, C.c_char_p, C.c_uint64, C.POINTER(P)]
+    lib.atp_state_open.argtypes = [P, C.c_char_p, C.POINTER(P), C.POINTER(C.c_uint64)]
+    lib.atp_state_release.argtypes = [P, P]
+    lib.atp_state_free.argtypes = [P, C.c_char_p]
+    lib.atp_state_put.argtypes = [P, C.c_char_p, P, C.c_uint64]
+    lib.atp_state_get.argtypes = [P, C.c_char_p, P, C.c_uint64, C.POINTER(C.c_uint64)]
+    lib.atp_state_list.argtypes = [P, C.c_char_p, C.c_uint64, C.POINTER(C.c_uint64)]
+    lib.atp_state_shutdown.argtypes = [P]
     lib.atp_last_error.restype = C.c_char_p
     for f in EXPORTS:
-        if f not in ("atp_plan_free", "atp_last_error", "atp_st_close"):
+        if f not in ("atp_plan_free", "atp_last_error", "atp_st_close", "atp_state_disconnect"):
             getattr(lib, f).restype = C.c_int
     return lib
 

@@ -43,7 +43,7 @@ def build_atp(out_dir: str | None = None, lib_path: str = LIB, defines=()) -> st
     os.makedirs(out_dir, exist_ok=True)
     dflags = ["-D" + d for d in defines]
     objs = []
-    for src in ("plan.cpp", "loader.cpp", "kvbudget.cpp", "capi.cpp"):
+    for src in ("plan.cpp", "loader.cpp", "kvbudget.cpp", "state.cpp", "capi.cpp"):
         obj = os.path.join(out_dir, src + ".o")
         _run(["g++", *HOST_FLAGS, *dflags, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)

@@ -11,6 +11,7 @@
 #include "kvbudget.h"
 #include "loader.h"
 #include "plan.h"
+#include "state.h"
 
 struct atp_plan_obj {
   atp::Plan *p;
@@ -18,6 +19,10 @@ struct atp_plan_obj {
 
 struct atp_st_obj {
   atp::StFiles *f;
+};
+
+struct atp_state_obj {
+  atp::StateConn *c;
 };
 
 namespace {
@@ -318,6 +323,100 @@ int atp_kv_evict_lru(const int32_t *table, int32_t n_seq, int32_t max_blocks, in
   return guard([&]() -> int {
     atp::evict_lru(table, n_seq, max_blocks, num_blocks, last_use, block_bytes, budget_bytes, compact != 0, keep,
                    new_table, stats);
+    return ATP_OK;
+  });
+}
+
+int atp_daemon_serve(const char *socket_path, int32_t device) {
+  return guard([&]() -> int { return atp::daemon_serve(socket_path, device); });
+}
+
+int atp_state_connect(const char *socket_path, atp_state_t **out) {
+  return guard([&]() -> int {
+    if (!out) return fail(ATP_EINVAL, "out is NULL");
+    *out = new atp_state_obj{atp::state_connect(socket_path)};
+    return ATP_OK;
+  });
+}
+
+void atp_state_disconnect(atp_state_t *s) {
+  if (!s) return;
+  atp::state_disconnect(s->c);
+  delete s;
+}
+
+int atp_state_alloc(atp_state_t *s, const char *name, uint64_t bytes, void **dev_ptr) {
+  return guard([&]() -> int {
+    if (!s || !dev_ptr) return fail(ATP_EINVAL, "state or dev_ptr is NULL");
+    *dev_ptr = atp::state_alloc(*s->c, name, bytes);
+    return ATP_OK;
+  });
+}
+
+int atp_state_open(atp_state_t *s, const char *name, void **dev_ptr, uint64_t *bytes) {
+  return guard([&]() -> int {
+    if (!s || !dev_ptr) return fail(ATP_EINVAL, "state or dev_ptr is NULL");
+    *dev_ptr = atp::state_open(*s->c, name, bytes);
+    return ATP_OK;
+  });
+}
+
+int atp_state_release(atp_state_t *s, void *dev_ptr) {
+  return guard([&]() -> int {
+    if (!s) return fail(ATP_EINVAL, "state is NULL");
+    atp::state_release(*s->c, dev_ptr);
+    return ATP_OK;
+  });
+}
+
+int atp_state_free(atp_state_t *s, const char *name) {
+  return guard([&]() -> int {
+    if (!s) return fail(ATP_EINVAL, "state is NULL");
+    atp::state_free(*s->c, name);
+    return ATP_OK;
+  });
+}
+
+int atp_state_put(atp_state_t *s, const char *name, const void *data, uint64_t bytes) {
+  return guard([&]() -> int {
+    if (!s) return fail(ATP_EINVAL, "state is NULL");
+    atp::state_put(*s->c, name, data, bytes);
+    return ATP_OK;
+  });
+}
+
+int atp_state_get(atp_state_t *s, const char *name, void *data, uint64_t cap, uint64_t *bytes) {
+  return guard([&]() -> int {
+    if (!s) return fail(ATP_EINVAL, "state is NULL");
+    uint64_t n = 0;
+    try {
+      n = atp::state_get(*s->c, name, data, cap);
+    } catch (const atp::Error &e) {
+      if (e.code == ATP_ECAPACITY && bytes) *bytes = atp::state_get(*s->c, name, nullptr, 0);
+      throw;
+    }
+    if (bytes) *bytes = n;
+    return ATP_OK;
+  });
+}
+
+int atp_state_list(atp_state_t *s, char *text, uint64_t cap, uint64_t *bytes) {
+  return guard([&]() -> int {
+    if (!s) return fail(ATP_EINVAL, "state is NULL");
+    std::string t = atp::state_list(*s->c);
+    if (bytes) *bytes = t.size() + 1;
+    if (text) {
+      if (cap < t.size() + 1) return fail(ATP_ECAPACITY, "text buffer too small");
+      memcpy(text, t.c_str(), t.size() + 1);
+    }
+    return ATP_OK;
+  });
+}
+
+int atp_state_shutdown(atp_state_t *s) {
+  return guard([&]() -> int {
+    if (!s) return fail(ATP_EINVAL, "state is NULL");
+    atp::state_shutdown(*s->c);
     return ATP_OK;
   });
 }
