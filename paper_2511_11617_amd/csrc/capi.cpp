@@ -256,11 +256,7 @@ int atp_plan_copies(const atp_plan_t *plan, int32_t which, atp_copy *out, int32_
   for (const atp::Chunk &ch : c.chunks) {
     for (const atp::HostCopy &h : ch.copies) v.push_back(host_copy(h, ATP_COPY_H2D_RING, -1, false));
     for (const atp::Launch &L : ch.scatters)
-      for (int d = L.d0; d < L.d1; ++d) {
-        atp_copy x = dev_copy(c.fams[d], ATP_COPY_SCATTER, -1);
-        x.after_d2h = ch.gate_pos;
-        v.push_back(x);
-      }
+      for (int d = L.d0; d < L.d1; ++d) v.push_back(dev_copy(c.fams[d], ATP_COPY_SCATTER, -1));
   }
   return copy_out(v, out, cap, n);
 }

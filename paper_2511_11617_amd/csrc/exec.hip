@@ -1,11 +1,12 @@
 // exec.hip — executor of the reshard library (Sec. III-C physical stage on
 // one GPU): uploads the plan's descriptors into the caller's staging
-// buffer, launches the prepare and repack kernels level by level on the
-// compute stream, lands the missing bytes from the pinned host buffer on the
-// copy stream (directly, or through the landing ring plus a scatter kernel),
-// reads dropped outbound bytes out before an in-place overwrite (on a side
-// stream that feeds a hardware queue of its own), and orders them with HIP
-// events.
+// buffer, launches the prepare and repack kernels level by level, lands the
+// missing bytes from the pinned host buffer (DMA copies straight into place
+// or through the landing ring plus a scatter kernel, or, in place, the copy
+// kernel reading the host buffer after the last level), reads dropped
+// outbound bytes out before an in-place overwrite (the copy kernel writing
+// the host buffer, on a side stream that feeds a hardware queue of its own),
+// and orders all of it with HIP events.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -42,8 +43,7 @@ struct CallState {
   size_t desc_cap = 0;
   int32_t *err_host = nullptr;  // pinned error word
   hipEvent_t start = nullptr;  // marks the caller's work queued before the call
-  hipEvent_t tail_compute = nullptr, tail_copy = nullptr, tail_d2h = nullptr;
-  hipEvent_t tail_late_copy = nullptr, tail_late_comp = nullptr;
+  hipEvent_t tail_compute = nullptr, tail_copy = nullptr, tail_side = nullptr;
   hipEvent_t rep0 = nullptr, rep1 = nullptr, h2d0 = nullptr, h2d1 = nullptr, d2h0 = nullptr, d2h1 = nullptr;
   struct LaunchRec {
     int kind, level;
@@ -464,14 +464,15 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   cs.start = start;
   HIPCHK(hipStreamWaitEvent(copy, start, 0));
 
-  // landings that depend on nothing go first, so that the link is busy at once
+  // direct landings wait for nothing (the planner routes every landing that
+  // would wait for a level or an outbound read elsewhere): they go first, so
+  // that the link is busy at once
   cs.h2d0 = E.ev_time();
   HIPCHK(hipEventRecord(cs.h2d0, copy));
-  for (const HostCopy &h : c.directs)
-    if (h.gate_pos == 0 && h.gate_level < 0) {
-      HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
-      cs.h2d_bytes += h.bytes;
-    }
+  for (const HostCopy &h : c.directs) {
+    HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
+    cs.h2d_bytes += h.bytes;
+  }
 
   // ---- upload descriptors, prepare ----------------------------------------------
   if (!c.fams.empty())
@@ -500,12 +501,12 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // stream that write straight into the pinned outbound buffer, in the
   // plan's order (by the first level that overwrites them), each level right
   // after the reads it needs; pos_ev[k] fires when the first k + 1 have
-  // finished.  That work and the weight inflow read after it stay off the
+  // finished (pos_ev.size() is the number of pieces issued).  That work and the weight inflow read after it stay off the
   // caller's streams, so that they do not hold up the other call's work
   // queued behind them.
   std::vector<hipEvent_t> pos_ev;
   const bool split = do_out && !kvcall;
-  hipStream_t late_copy = copy, late_comp = compute;
+  hipStream_t late_comp = compute;
   if (split) {
     late_comp = E.side;
     hipEvent_t prepared = E.ev_sync();  // the outbound launches read the descriptors
@@ -612,56 +613,41 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   }
 
   // ---- inflow ------------------------------------------------------------------------
-  auto gate_out = [&](hipStream_t s, int gate_pos) {
-    if (gate_pos > 0 && gate_pos <= int(pos_ev.size())) HIPCHK(hipStreamWaitEvent(s, pos_ev[gate_pos - 1], 0));
-  };
-  auto direct = [&](const HostCopy &h, hipStream_t s) {
-    if (h.gate_level >= 0 && level_end[h.gate_level]) HIPCHK(hipStreamWaitEvent(s, level_end[h.gate_level], 0));
-    gate_out(s, h.gate_pos);
-    HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, s));
-    cs.h2d_bytes += h.bytes;
-  };
-  // (ungated landings were issued first) those waiting for levels only
-  for (const HostCopy &h : c.directs)
-    if (h.gate_pos == 0 && h.gate_level >= 0) direct(h, late_copy);
-  // ring: H2D into a slot, scatter from it after every level (and after the
-  // outbound reads the chunk overwrites)
+  // (direct landings went first, none of them waits for anything)
+  // ring: H2D into a slot, then a scatter from it after every level; a chunk
+  // reuses its slot once the slot's previous scatter is done
   std::vector<hipEvent_t> slot_free(c.chunks.size(), nullptr);
   for (size_t i = 0; i < c.chunks.size(); ++i) {
     const Chunk &ch = c.chunks[i];
-    hipStream_t cs_copy = late_copy, cs_comp = late_comp;  // scatters after every level
     if (i >= size_t(c.n_slots) && slot_free[i - c.n_slots])
-      HIPCHK(hipStreamWaitEvent(cs_copy, slot_free[i - c.n_slots], 0));
+      HIPCHK(hipStreamWaitEvent(copy, slot_free[i - c.n_slots], 0));
     for (const HostCopy &h : ch.copies) {
-      HIPCHK(hipMemcpyAsync(b_st + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, cs_copy));
+      HIPCHK(hipMemcpyAsync(b_st + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
       cs.h2d_bytes += h.bytes;
     }
     hipEvent_t landed = E.ev_sync();
-    HIPCHK(hipEventRecord(landed, cs_copy));
-    HIPCHK(hipStreamWaitEvent(cs_comp, landed, 0));
-    gate_out(cs_comp, ch.gate_pos);
+    HIPCHK(hipEventRecord(landed, copy));
+    HIPCHK(hipStreamWaitEvent(late_comp, landed, 0));
     for (const Launch &L : ch.scatters) {
       CallState::LaunchRec r{2, -1, L.bytes, E.ev_time(), E.ev_time()};
-      HIPCHK(hipEventRecord(r.e0, cs_comp));
-      launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, cs_comp);
-      HIPCHK(hipEventRecord(r.e1, cs_comp));
+      HIPCHK(hipEventRecord(r.e0, late_comp));
+      launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
+      HIPCHK(hipEventRecord(r.e1, late_comp));
       cs.launches.push_back(r);
       cs.scatter_bytes += L.bytes;
     }
     slot_free[i] = E.ev_sync();
-    HIPCHK(hipEventRecord(slot_free[i], cs_comp));
+    HIPCHK(hipEventRecord(slot_free[i], late_comp));
   }
-  for (const HostCopy &h : c.directs)
-    if (h.gate_pos > 0) direct(h, late_copy);
   cs.h2d1 = E.ev_time();
   if (!c.host_reads.empty()) {
     // the inflow ends with the later of the copy stream and the host reads
     hipEvent_t copied = E.ev_sync();
-    HIPCHK(hipEventRecord(copied, late_copy));
+    HIPCHK(hipEventRecord(copied, copy));
     HIPCHK(hipStreamWaitEvent(late_comp, copied, 0));
     HIPCHK(hipEventRecord(cs.h2d1, late_comp));
   } else {
-    HIPCHK(hipEventRecord(cs.h2d1, late_copy));
+    HIPCHK(hipEventRecord(cs.h2d1, copy));
   }
 
   // ---- tails ----------------------------------------------------------------------
@@ -670,18 +656,12 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   HIPCHK(hipEventRecord(cs.tail_compute, compute));
   cs.tail_copy = E.ev_sync();
   HIPCHK(hipEventRecord(cs.tail_copy, copy));
-  cs.tail_d2h = cs.tail_late_copy = cs.tail_late_comp = nullptr;
+  cs.tail_side = nullptr;
   if (do_out) {
-    cs.tail_d2h = E.ev_sync();
-    HIPCHK(hipEventRecord(cs.tail_d2h, E.side));
-  }
-  if (split) {
-    // the late streams are not joined back into the caller's streams (that
-    // would hold up the other call's work); atp_sync waits for them
-    cs.tail_late_copy = E.ev_sync();
-    HIPCHK(hipEventRecord(cs.tail_late_copy, late_copy));
-    cs.tail_late_comp = E.ev_sync();
-    HIPCHK(hipEventRecord(cs.tail_late_comp, late_comp));
+    // the side stream is not joined back into the caller's streams (that
+    // would hold up the other call's work); atp_sync waits for it
+    cs.tail_side = E.ev_sync();
+    HIPCHK(hipEventRecord(cs.tail_side, E.side));
   }
   cs.pending = true;
 }
@@ -705,7 +685,7 @@ int exec_sync(Plan &P, atp_timing *out) {
   for (int which = 0; which < 2; ++which) {
     CallState &cs = which == 0 ? E.w : E.k;
     if (!cs.pending) continue;
-    for (hipEvent_t e : {cs.tail_compute, cs.tail_copy, cs.tail_d2h, cs.tail_late_copy, cs.tail_late_comp}) {
+    for (hipEvent_t e : {cs.tail_compute, cs.tail_copy, cs.tail_side}) {
       if (!e) continue;
       hipError_t err = hipEventSynchronize(e);
       if (err != hipSuccess && rc == ATP_OK) {
@@ -785,7 +765,7 @@ void exec_free(Plan &P) {
     // drain anything still queued before the pinned buffers go away
     for (CallState *c : {&E->w, &E->k})
       if (c->pending)
-        for (hipEvent_t e : {c->tail_compute, c->tail_copy, c->tail_d2h, c->tail_late_copy, c->tail_late_comp})
+        for (hipEvent_t e : {c->tail_compute, c->tail_copy, c->tail_side})
           if (e) (void)hipEventSynchronize(e);
     delete E;
     P.exec = nullptr;

@@ -1065,8 +1065,8 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
     if (P.inplace && !kvcall) oidx.query(d, [&](int o) { k = std::max(k, pos[o] + 1); });
     return k;
   };
-  std::vector<std::pair<int, const Pending *>> ring;  // (outbound gate, piece)
-  std::vector<Fam> host_pieces;                        // in place: read by the copy kernel
+  std::vector<const Pending *> ring;  // through the landing ring
+  std::vector<Fam> host_pieces;       // in place: read by the copy kernel
   uint64_t ring_total = 0, max_item = 0;
   for (const Pending &pd : inflow) {
     // Only large contiguous gaps land directly: every copy command costs the
@@ -1101,18 +1101,16 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
       f.flags = (f.flags & ~(3u << DF_SRC_SHIFT)) | (BUF_IN << DF_SRC_SHIFT);
       host_pieces.push_back(f);
     } else {
+      // out of place, or the KV call in place: nothing here is read by an
+      // outbound copy (KV outbound is gathered at level 0), and the scatters
+      // run after every level
       const Fam &f = pd.fam;
-      int g = (f.flags & DF_DST_IND) ? 0 : out_gate(dst_span(f, f.o_begin, f.o_end));
-      ring.push_back({g, &pd});
+      ring.push_back(&pd);
       ring_total += f.bytes();
       max_item = std::max<uint64_t>(max_item, f.rows * f.run);
     }
   }
   if (!host_pieces.empty()) emit_group(c, host_pieces, c.n_levels, 4, c.host_reads, live_hint);
-  std::stable_sort(ring.begin(), ring.end(),
-                   [](const std::pair<int, const Pending *> &a, const std::pair<int, const Pending *> &b) {
-                     return a.first < b.first;
-                   });
 
   uint64_t slot = 0;
   if (!ring.empty()) {
@@ -1142,20 +1140,16 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
       ch = Chunk();
       fill = 0;
     };
-    for (const auto &gp : ring) {
-      const Pending *pd = gp.second;
+    for (const Pending *pd : ring) {
       const Fam &f = pd->fam;
       uint64_t item = f.rows * f.run;
       int64_t k = f.o_begin;
-      // gated pieces start a chunk of their own kind
-      if (!pieces.empty() && (ch.gate_pos > 0) != (gp.first > 0)) flush();
       while (k < f.o_end) {
         int64_t room = int64_t((slot - fill) / item);
         if (room <= 0) {
           flush();
           continue;
         }
-        ch.gate_pos = std::max(ch.gate_pos, gp.first);
         int64_t k1 = std::min<int64_t>(f.o_end, k + room);
         // host copy of items [k, k1) into the slot at `fill`
         uint64_t hoff = pd->host_off + uint64_t(k - f.o_begin) * item;

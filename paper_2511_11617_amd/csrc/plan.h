@@ -71,9 +71,11 @@ struct HostCopy {
   uint64_t dev_off = 0;       // device offset (arena or staging slot)
   uint64_t bytes = 0;
   int dev_buf = BUF_OUT;      // BUF_OUT for direct landing, BUF_STAGE ring
-  int gate_level = -1;        // in place: level whose reads must finish
-  int gate_pos = 0;           // in place: the first gate_pos outbound copies
-                              // (in issue order) must finish first
+  // while planning a landing in place: the last level that reads its
+  // destination and the number of outbound copies (in issue order) that must
+  // finish first; a planned direct landing always has neither
+  int gate_level = -1;
+  int gate_pos = 0;
   // strided device side (outbound): rows x run at dev pitch
   uint64_t rows = 1, run = 0, dev_pitch = 0;
 };
@@ -81,7 +83,6 @@ struct HostCopy {
 // Landing-ring chunk: H2D into a slot, then scatter launch(es) from it.
 struct Chunk {
   int slot = 0;
-  int gate_pos = 0;               // outbound copies its scatter must wait for
   std::vector<HostCopy> copies;   // into the slot
   std::vector<Launch> scatters;   // aligned and/or 2-byte-granular
 };
