@@ -71,11 +71,23 @@ def parse():
                     help="repeat the CPU oracle over the whole workload for at least this long")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="also run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--inplace", action="store_true",
+                    help="reshard the workload in place (the new shard over the old one), whatever it states")
+    ap.add_argument("--state", action="store_true",
+                    help="run the workload in place on memory the state plane holds: a writer process "
+                         "allocates one weight and one KV region per layer group through the daemon and "
+                         "exits; this process maps them (timed) and reshards group after group")
+    ap.add_argument("--state-groups", type=int, default=0,
+                    help="layer groups of the state leg (default: the fewest whose regions fit)")
+    ap.add_argument("--state-writer", default=None, help=argparse.SUPPRESS)
+    ap.add_argument("--state-regions", default="", help=argparse.SUPPRESS)
     return ap.parse_args()
 
 
 def main():
     args = parse()
+    if args.state_writer:
+        return state_writer(args)
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark measures one GPU's share of the reshard; "
                                    "run it with --gpus 1 (multi-GPU runs are not part of it)"}))
@@ -87,7 +99,9 @@ def main():
     from synth.content import TAGS, Content
     from synth.pinned import Pinned
 
-    cfg = configs.get(args.workload)
+    if args.state:
+        return state_main(args)
+    cfg = configs.get(args.workload, **({"inplace": True} if args.inplace else {}))
     table, pool = pagetable.make_for(cfg)
     n_live = int(len(np.unique(table[table >= 0])))
     inplace = bool(cfg["inplace"])
@@ -234,23 +248,11 @@ def main():
     value = alg / (rep_ms * 1e-3) / 1e9 if rep_ms > 0 else 0.0  # Full Reload keeps nothing
     wall_ms = elapsed / K * 1e3
     h2d_ms = sum(t.h2d_ms for t in recs) / K
-    # dominant kernel: the repack launch moving the most bytes
-    per = {}
-    for L in launches:
-        for kind, level, b, ms in L:
-            if kind in (0, 1):
-                per.setdefault((kind, level, b), []).append(ms)
-    (dk, dl, db), dms = max(per.items(), key=lambda kv: kv[0][2]) if per else ((0, 0, 0), [0.0])
+    dk, db, dom_ms, dom_gbps, kernels = dominant_launch(launches)
     traffic = None
     counted = COUNTED_TRAFFIC.get(cfg["name"])
-    if counted and args.plan == "cm" and kernel_src_hash() == COUNTED_TRAFFIC["src"]:
+    if counted and args.plan == "cm" and not args.inplace and kernel_src_hash() == COUNTED_TRAFFIC["src"]:
         traffic = counted.get("weights" if dk == 0 else "kv")
-    dom_ms = sum(dms) / len(dms)
-    dom_gbps = 2 * db / (dom_ms * 1e-3) / 1e9 if dom_ms > 0 else 0.0
-    kernels = [{"call": "weights" if k == 0 else "kv",
-                "level": l, "alg_bytes": 2 * b, "avg_ms": round(sum(v) / len(v), 4),
-                "GBps": round(2 * b / (sum(v) / len(v) * 1e-3) / 1e9, 1)}
-               for (k, l, b), v in sorted(per.items())][:8]
 
     out = {
         "metric": "reshard GB/s (fraction of HBM peak) + wall ms per TP k→k-1; reload bytes vs min",
@@ -305,6 +307,230 @@ def main():
             torch.cuda.synchronize()
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, aw, ak, hin_w.tensor, hin_k.tensor,
                                            table, pool)
+    print(json.dumps(out), flush=True)
+
+
+def dominant_launch(launches):
+    """The repack launch that moves the most bytes, averaged over the steps:
+    (call kind, bytes moved, ms, algorithmic GB/s, table of the launches)."""
+    per = {}
+    for L in launches:
+        for kind, level, b, ms in L:
+            if kind in (0, 1):
+                per.setdefault((kind, level, b), []).append(ms)
+    (dk, dl, db), dms = max(per.items(), key=lambda kv: kv[0][2]) if per else ((0, 0, 0), [0.0])
+    dom_ms = sum(dms) / len(dms)
+    dom_gbps = 2 * db / (dom_ms * 1e-3) / 1e9 if dom_ms > 0 else 0.0
+    kernels = [{"call": "weights" if k == 0 else "kv",
+                "level": l, "alg_bytes": 2 * b, "avg_ms": round(sum(v) / len(v), 4),
+                "GBps": round(2 * b / (sum(v) / len(v) * 1e-3) / 1e9, 1)}
+               for (k, l, b), v in sorted(per.items())][:8]
+    return dk, db, dom_ms, dom_gbps, kernels
+
+
+def state_writer(args):
+    """The process that held the old shard: asks the daemon for the regions,
+    leaves the block table with it, and exits without any cleanup.  The
+    regions' bytes are what the allocation left there: moving bytes costs
+    the same whatever they are (the state-plane tests check content)."""
+    from paper_2511_11617_amd import state
+    from synth import configs, pagetable
+
+    cl = state.Client(args.state_writer)
+    for item in args.state_regions.split(","):
+        name, n = item.split(":")
+        cl.alloc(name, int(n))
+    table, _ = pagetable.make_for(configs.get(args.workload))
+    cl.put("kv.table", table.astype(np.int32))
+    cl.put("kv.shape", np.array(table.shape, np.int64))
+    log(f"[writer] {len(args.state_regions.split(','))} regions allocated; exiting without cleanup")
+    os._exit(3)
+
+
+def state_main(args):
+    """The workload in place on device memory the state plane owns
+    (Sec. III-A).  IPC regions stay under 2 GiB, so the layers are split into
+    the fewest balanced groups whose weight and KV regions fit; every layer
+    group is a reshard of its own (layers are independent in the plan), run
+    one after the other with a fresh plan each.  Timed: the attach (connect,
+    open every region, fetch the block table) once, and every step."""
+    import subprocess
+    import tempfile
+
+    import torch
+
+    from paper_2511_11617_amd import atp, problem, state
+    from synth import configs, pagetable
+    from synth.pinned import Pinned
+
+    cfg = configs.get(args.workload, inplace=True)
+    table, pool = pagetable.make_for(cfg)
+    n_live = int(len(np.unique(table[table >= 0])))
+    cap = cfg["staging_cap"] or 0
+    L = cfg["layers"]
+    built, stats = {}, {}
+
+    def sizes(layers):
+        if layers not in built:
+            built[layers] = problem.build(dict(cfg, layers=layers), n_live=n_live, pool=pool,
+                                          flags=atp.INPLACE, staging_cap=cap)
+            st = built[layers].plan().stats()
+            stats[layers] = st
+        st = stats[layers]
+        return max(st.old_arena_bytes, st.new_arena_bytes, 256), max(st.old_kv_bytes, st.new_kv_bytes, 256)
+
+    def split(n):
+        return [L // n + (i < L % n) for i in range(n)]
+
+    def fits(n):
+        return all(max(sizes(g)) <= state.MAX_REGION for g in set(split(n)))
+
+    if args.state_groups:
+        n_groups = args.state_groups
+        if not 1 <= n_groups <= L or not fits(n_groups):
+            raise SystemExit(f"{n_groups} layer groups do not give regions under {state.MAX_REGION} bytes")
+    else:
+        n_groups = next((n for n in range(1, L + 1) if fits(n)), 0)
+        if not n_groups:
+            raise SystemExit("one layer's arena exceeds the state plane's region limit")
+    groups = split(n_groups)
+    regions = []
+    for i, g in enumerate(groups):
+        wb, kb = sizes(g)
+        regions += [(f"w{i}", wb), (f"k{i}", kb)]
+    log(f"[state] workload {args.workload} {cfg['name']} in place: {n_groups} layer groups {groups}, "
+        f"{len(regions)} regions, {sum(n for _, n in regions) / 1e9:.2f} GB")
+
+    dev = torch.device("cuda")
+    u8 = torch.uint8
+    sts = [stats[g] for g in set(groups)]
+    stage_w = torch.empty(max(max(s.staging_w for s in sts), 256), dtype=u8, device=dev)
+    stage_k = torch.empty(max(max(s.staging_kv for s in sts), 256), dtype=u8, device=dev)
+    # one host buffer of each kind serves every group in turn: the groups run
+    # one after the other, and what the bytes are does not change the cost
+    hin_w = Pinned(max(s.inflow_w for s in sts))
+    hin_k = Pinned(max(s.inflow_kv for s in sts))
+    hout_w = Pinned(max(s.outbound_w for s in sts))
+    hout_k = Pinned(max(s.outbound_kv for s in sts))
+    torch.cuda.synchronize()
+
+    d = tempfile.mkdtemp(prefix="atp-", dir="/tmp")
+    sock = os.path.join(d, "s.sock")
+    daemon = state.spawn(sock)
+    cl = None
+    try:
+        r = subprocess.run([sys.executable, os.path.abspath(__file__), "--state-writer", sock,
+                            "--workload", str(args.workload),
+                            "--state-regions", ",".join(f"{n}:{b}" for n, b in regions)],
+                           capture_output=True, text=True, timeout=600)
+        if r.returncode != 3:
+            raise RuntimeError(f"state writer failed ({r.returncode}): {r.stderr[-2000:]}")
+        t0 = time.perf_counter()
+        cl = state.Client(sock)
+        mapped = [(cl.open(f"w{i}"), cl.open(f"k{i}")) for i in range(n_groups)]
+        shape = tuple(int(x) for x in cl.get_array("kv.shape", np.int64))
+        tab = cl.get_array("kv.table", np.int32, shape)
+        attach_ms = (time.perf_counter() - t0) * 1e3
+        if not np.array_equal(tab, table):
+            raise RuntimeError("the block table the daemon returned differs from the workload's")
+        for (pw, wb), (pk, kb) in mapped:
+            if pw % 256 or pk % 256:
+                raise RuntimeError("a mapped region is not 256-byte aligned")
+        log(f"[state] attach: {attach_ms:.2f} ms for {len(regions)} regions and the block table")
+        table_d = torch.from_numpy(tab).to(dev)
+        compute = torch.cuda.current_stream()
+        copy = torch.cuda.Stream()
+
+        def step():
+            recs = []
+            for i, g in enumerate(groups):
+                st = stats[g]
+                (pw, wb), (pk, kb) = mapped[i]
+                p = built[g].plan()
+                p.reshard_weights(pw, wb, None, 0, hin_w.ptr, st.inflow_w, hout_w.ptr, st.outbound_w,
+                                  stage_w.data_ptr(), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
+                p.reshard_kv(pk, kb, None, 0, table_d.data_ptr(), shape[0], shape[1], hin_k.ptr,
+                             st.inflow_kv, hout_k.ptr, st.outbound_kv, stage_k.data_ptr(), stage_k.numel(),
+                             compute.cuda_stream, copy.cuda_stream)
+                recs.append((p.sync(), [(x.kind, x.level, x.bytes, x.ms) for x in p.launches()]))
+            return recs
+
+        for i in range(args.warmup):
+            step()
+            log(f"[state] warmup {i + 1}/{args.warmup} done")
+        steps, elapsed = [], 0.0
+        for i in range(args.steps):
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            recs = step()
+            torch.cuda.synchronize()
+            elapsed += time.perf_counter() - t1
+            steps.append(recs)
+            log(f"[state] step {i + 1}/{args.steps}: walls " +
+                " ".join(f"{t.wall_ms:.1f}" for t, _ in recs) + " ms, repack " +
+                f"{sum(t.repack_union_ms for t, _ in recs):.3f} ms")
+        for ptr_w, ptr_k in mapped:
+            cl.release(ptr_w[0])
+            cl.release(ptr_k[0])
+        for n, _ in regions:
+            cl.free(n)
+    finally:
+        try:
+            c = cl or state.Client(sock)
+            c.shutdown()
+            c.close()
+        except atp.AtpError:
+            pass
+        try:
+            daemon.wait(timeout=60)
+        except subprocess.TimeoutExpired:
+            daemon.kill()
+            daemon.wait()
+        if os.path.isdir(d) and not os.listdir(d):
+            os.rmdir(d)
+
+    K = args.steps
+    moved = sum(stats[g].moved_w + stats[g].moved_kv for g in groups)
+    inflow = sum(stats[g].inflow_w + stats[g].inflow_kv for g in groups)
+    rep_ms = sum(sum(t.repack_union_ms for t, _ in recs) for recs in steps) / K
+    wall_ms = elapsed / K * 1e3
+    value = 2 * moved / (rep_ms * 1e-3) / 1e9 if rep_ms > 0 else 0.0
+    dk, db, dom_ms, dom_gbps, kernels = dominant_launch([L_ for recs in steps for _, L_ in recs])
+    out = {
+        "metric": "reshard GB/s (fraction of HBM peak) + wall ms per TP k→k-1; reload bytes vs min",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": cfg["name"] + " in place on state-plane regions", "layers": L,
+                   "hidden": cfg["hidden"], "tp": f"{cfg['old_tp']}->{cfg['new_tp']}", "failed": cfg["failed"],
+                   "self_old_rank": cfg["self_old"], "kv_sequences": cfg["n_seq"],
+                   "seq_tokens": cfg["seq_tokens"], "in_place": True, "planner": "cm"},
+        "state": {"layer_groups": groups, "regions": len(regions),
+                  "region_bytes": [b for _, b in regions], "region_limit": state.MAX_REGION,
+                  "attach_ms": round(attach_ms, 3),
+                  "writer": "separate process; allocated through the daemon and exited without cleanup"},
+        "hbm_frac": round(value / HBM_PEAK_GBPS, 4),
+        "repack_ms": round(rep_ms, 4),
+        "wall_ms": round(wall_ms, 3),
+        "group_wall_ms": [round(sum(recs[i][0].wall_ms for recs in steps) / K, 3) for i in range(n_groups)],
+        "plan_ms": round(sum(sum(t.plan_ms for t, _ in recs) for recs in steps) / K, 3),
+        "h2d_ms": round(sum(sum(t.h2d_ms for t, _ in recs) for recs in steps) / K, 3),
+        "moved_bytes": int(moved),
+        "inflow_bytes": int(inflow),
+        "kernels": kernels,
+        "roofline": {"bound": "hbm", "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "k_copy16", "call": "weights" if dk == 0 else "kv",
+                     "alg_bytes_per_launch": int(2 * db), "avg_launch_ms": round(dom_ms, 4)},
+    }
     print(json.dumps(out), flush=True)
 
 

@@ -35,6 +35,8 @@ def case(name: str):
         return configs.get(1)
     if name == "dense80-2l":
         return configs.scaled(5, layers=2, n_seq=2, seq_tokens=256)
+    if name == "dense40-2l":
+        return configs.scaled(2, layers=2, n_seq=2, seq_tokens=256, inplace=True)
     raise ValueError(name)
 
 

@@ -43,8 +43,8 @@ def _check(name, got, want, valid):
     assert bad.size == 0, f"{name}: {bad.size} of {valid.sum()} sampled words wrong"
 
 
-def run_full(n):
-    c = configs.get(n)
+def run_full(n, inplace=None):
+    c = configs.get(n, **({} if inplace is None else {"inplace": inplace}))
     pb = model.build(c)
     content = Content(c["seed"], c["w_kind"], c["kv_kind"])
     table, pool = pagetable.make_for(c)
@@ -151,3 +151,9 @@ def run_full(n):
 @pytest.mark.parametrize("n", [5, 4, 3, 2])   # the largest pinned buffers first
 def test_full_size_workload(n):
     run_full(n)
+
+
+def test_full_size_workload_2_in_place():
+    """The headline shape resharded over its own old shard (what the state
+    plane's regions hold)."""
+    run_full(2, inplace=True)

@@ -60,10 +60,11 @@ def test_random_small_in_place(seed):
     run_case(c, flags=atp.INPLACE, name=f"random-inplace-{seed}")
 
 
+@pytest.mark.parametrize("inplace", [False, True])
 @pytest.mark.parametrize("n", [2, 3, 4])
-def test_large_shapes_one_layer(n):
+def test_large_shapes_one_layer(n, inplace):
     c = configs.scaled(n, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
-    run_case(c, name=f"cfg{n}-1layer")
+    run_case(c, flags=atp.INPLACE if inplace else 0, name=f"cfg{n}-1layer" + ("-inplace" if inplace else ""))
 
 
 def test_cfg5_shape_in_place_two_layers():

@@ -81,10 +81,11 @@ def test_random_small(seed, experts, inplace):
 
 
 @pytest.mark.slow
+@pytest.mark.parametrize("inplace", [False, True])
 @pytest.mark.parametrize("n", [2, 3, 4])
-def test_large_shapes_one_layer(n):
+def test_large_shapes_one_layer(n, inplace):
     c = configs.scaled(n, layers=1, n_seq=2, seq_tokens=128, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
-    sim_case(c)
+    sim_case(c, flags=atp.INPLACE if inplace else 0)
 
 
 @pytest.mark.slow
