@@ -71,6 +71,8 @@ def parse():
                     help="repeat the CPU oracle over the whole workload for at least this long")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="also run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--self-old", type=int, default=None,
+                    help="measure this surviving old rank's share instead of the workload's named one")
     ap.add_argument("--inplace", action="store_true",
                     help="reshard the workload in place (the new shard over the old one), whatever it states")
     ap.add_argument("--state", action="store_true",
@@ -101,7 +103,14 @@ def main():
 
     if args.state:
         return state_main(args)
-    cfg = configs.get(args.workload, **({"inplace": True} if args.inplace else {}))
+    over = {}
+    if args.inplace:
+        over["inplace"] = True
+    if args.self_old is not None:
+        over["self_old"] = args.self_old
+    cfg = configs.get(args.workload, **over)
+    if not 0 <= cfg["self_old"] < cfg["old_tp"] or cfg["self_old"] in cfg["failed"]:
+        raise SystemExit(f"old rank {cfg['self_old']} is not a survivor of workload {args.workload}")
     table, pool = pagetable.make_for(cfg)
     n_live = int(len(np.unique(table[table >= 0])))
     inplace = bool(cfg["inplace"])
@@ -127,6 +136,20 @@ def main():
     built = problem.build(cfg, n_live=n_live, pool=pool, flags=flags, staging_cap=cap)
     plan = built.plan()
     st = plan.stats()
+    # which survivor hosts which new rank: the paper's in-order choice against
+    # the permutation that keeps the most bytes (host planning only)
+    assignment = {}
+    for nm, fl in (("inorder", atp.ASSIGN_INORDER), ("maxretain", atp.ASSIGN_MAXRETAIN)):
+        try:
+            a = problem.build(cfg, n_live=n_live, pool=pool, flags=(flags & ~atp.ASSIGN_MAXRETAIN) | fl,
+                              staging_cap=cap).plan().stats()
+            assignment[nm] = {"self_new_rank": int(a.self_new_rank),
+                              "self_inflow_bytes": int(a.inflow_w + a.inflow_kv),
+                              "self_retained_bytes": int(a.retained_w + a.retained_kv),
+                              "global_retained_bytes": int(a.global_keep),
+                              "global_reload_bytes": int(a.global_reload)}
+        except atp.AtpError as e:
+            assignment[nm] = {"error": str(e)}
     dev = torch.device("cuda")
     u8 = torch.uint8
     content = Content(cfg["seed"], cfg["w_kind"], cfg["kv_kind"])
@@ -286,6 +309,9 @@ def main():
         "wall_vs_h2d_bound": round((st.inflow_w + st.inflow_kv) / (h2d_peak * 1e9) * 1e3 / wall_ms, 3)
         if h2d_peak else None,
         "overlap": round(sum(t.overlap for t in recs) / K, 3),
+        "scatter_ms": round(sum(t.scatter_ms for t in recs) / K, 4),
+        "scatter_bytes": int(recs[-1].scatter_bytes),  # landing ring -> place, not algorithmic
+        "assignment": assignment,
         "retained_bytes": int(st.retained_w + st.retained_kv),
         "moved_bytes": int(st.moved_w + st.moved_kv),
         "inflow_bytes": int(st.inflow_w + st.inflow_kv),

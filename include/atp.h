@@ -170,10 +170,11 @@ void atp_plan_free(atp_plan_t *plan);
  *                (in place only) the old bytes peers need and this GPU drops,
  *                read before they are overwritten; may be NULL if 0 bytes
  *   staging      device scratch of at least stats.staging_w bytes
- * With ATP_INPLACE the copy kernel itself writes the outbound bytes and
- * reads the inflow that must wait for a level or an outbound read: both
- * host buffers must then come from hipHostMalloc (device-accessible at the
- * same address) and be 256-byte aligned, else ATP_EINVAL / ATP_EALIGN.
+ * The copy kernel itself reads every inflow piece that is not a large
+ * contiguous gap (those land by DMA) from inflow_host, and with ATP_INPLACE
+ * writes the outbound bytes: both host buffers must come from hipHostMalloc
+ * (device-accessible at the same address) and be 256-byte aligned, else
+ * ATP_EINVAL / ATP_EALIGN.
  * Launch errors return ATP_EHIP; kernel-side errors surface in atp_sync. */
 int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes,
                         void *new_arena, uint64_t new_arena_bytes,
@@ -280,8 +281,8 @@ int atp_plan_segments(const atp_plan_t *plan, int32_t which, atp_segment *out,
                       int32_t cap, int32_t *n);
 
 /* One kernel launch of the last reshard: kind 0 = weight repack,
- * 1 = KV repack, 2 = landing-ring scatter, 3 = outbound read into the host
- * buffer (in place), 4 = inflow read from the host buffer (in place);
+ * 1 = KV repack, 2 = landing-ring scatter (in-place KV inflow), 3 = outbound
+ * read into the host buffer (in place), 4 = inflow read from the host buffer;
  * `ms` from HIP events on the stream the launch ran on. */
 typedef struct {
   int32_t kind, level;

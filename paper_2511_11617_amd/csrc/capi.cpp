@@ -242,13 +242,14 @@ int atp_plan_copies(const atp_plan_t *plan, int32_t which, atp_copy *out, int32_
     x.after_d2h = h.gate_pos;
     v.push_back(x);
   }
-  // in place: inflow the copy kernel reads from the host buffer after the
-  // last level and after every outbound read of the call
+  // inflow the copy kernel reads from the host buffer: in place after the
+  // last level and after every outbound read of the call, out of place at
+  // any time
   int32_t n_d2h = 0;
   for (const atp_copy &x : v) n_d2h += x.op == ATP_COPY_D2H && x.src_buf != ATP_BUF_STAGING;
   for (const atp::Launch &L : c.host_reads)
     for (int d = L.d0; d < L.d1; ++d) {
-      atp_copy x = dev_copy(c.fams[d], ATP_COPY_H2D, c.n_levels > 0 ? c.n_levels - 1 : -1);
+      atp_copy x = dev_copy(c.fams[d], ATP_COPY_H2D, P.inplace && c.n_levels > 0 ? c.n_levels - 1 : -1);
       x.src_buf = ATP_BUF_INFLOW;
       x.after_d2h = n_d2h;
       v.push_back(x);

@@ -1,12 +1,14 @@
 // exec.hip — executor of the reshard library (Sec. III-C physical stage on
 // one GPU): uploads the plan's descriptors into the caller's staging
 // buffer, launches the prepare and repack kernels level by level, lands the
-// missing bytes from the pinned host buffer (DMA copies straight into place
-// or through the landing ring plus a scatter kernel, or, in place, the copy
-// kernel reading the host buffer after the last level), reads dropped
-// outbound bytes out before an in-place overwrite (the copy kernel writing
-// the host buffer, on a side stream that feeds a hardware queue of its own),
-// and orders all of it with HIP events.
+// missing bytes from the pinned host buffer (DMA copies of large contiguous
+// gaps straight into place; every other piece read by the copy kernel from
+// the host buffer, out of place beside the repack on a side stream that
+// feeds a hardware queue of its own, in place after the last level; the
+// in-place KV inflow through the landing ring plus a scatter kernel), reads
+// dropped outbound bytes out before an in-place overwrite (the copy kernel
+// writing the host buffer, on the side stream), and orders all of it with
+// HIP events.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -45,6 +47,7 @@ struct CallState {
   hipEvent_t start = nullptr;  // marks the caller's work queued before the call
   hipEvent_t tail_compute = nullptr, tail_copy = nullptr, tail_side = nullptr;
   hipEvent_t rep0 = nullptr, rep1 = nullptr, h2d0 = nullptr, h2d1 = nullptr, d2h0 = nullptr, d2h1 = nullptr;
+  hipEvent_t hr1 = nullptr;  // end of the copy kernel's host reads (inflow ends with the later of h2d1, hr1)
   struct LaunchRec {
     int kind, level;
     uint64_t bytes;
@@ -71,8 +74,9 @@ struct Exec {
   int grid_max = 2048;
   // In place: `side` runs the outbound gathers and their device-to-host
   // copies, the weight levels that wait for them and the weight inflow the
-  // copy kernel reads after them.  It feeds another hardware queue than the
-  // caller's streams and is shared process-wide (choose_side).
+  // copy kernel reads after them.  Out of place it runs the copy kernel's
+  // host reads.  It feeds another hardware queue than the caller's streams
+  // and is shared process-wide (choose_side).
   hipStream_t side = nullptr;
   hipStream_t side_for_compute = nullptr, side_for_copy = nullptr;
   std::vector<hipEvent_t> sync_pool, time_pool;
@@ -174,12 +178,20 @@ constexpr uint32_t kSpinIters = 400;     // about 1.4 ms at 2.4 GHz
 constexpr float kSpinMarginMs = 0.3f;    // the empty kernel must finish this much earlier
 
 // Workgroups of the launches that move bytes over PCIe with the copy kernel
-// (persistent grids over their tiles).  64 already carry a full x16 Gen5
-// link from pinned host memory.  The outbound reads get a narrow grid: wide
-// device-to-host writers (the runtime's 512-workgroup blits) slowed a
-// concurrent HBM-bound repack several-fold; 8 workgroups leave a concurrent
-// HBM copy at full speed while writing 17 GB/s beside it (41 GB/s alone).
-constexpr uint64_t kHostReadGrid = 128;
+// (persistent grids over their tiles).  Host reads: 32 workgroups carry a
+// full x16 Gen5 link from pinned host memory (57 GB/s; 16 reach 50).  The
+// long-latency host reads they keep in flight slow an HBM-bound repack
+// running beside them, the more the wider the grid: the 40-layer TP 4->3
+// repack ran at 6.14 / 5.97 / 5.55 / 2.63 / 1.12 TB/s beside 32 / 48 / 64 /
+// 80 / 128 host-read workgroups (6.2 alone).  The outbound reads get a narrow
+// grid: wide device-to-host writers (the runtime's 512-workgroup blits)
+// slowed a concurrent HBM-bound repack several-fold; 8 workgroups leave a
+// concurrent HBM copy at full speed while writing 17 GB/s beside it (41 GB/s
+// alone).
+#ifndef ATP_HOST_READ_GRID
+#define ATP_HOST_READ_GRID 32
+#endif
+constexpr uint64_t kHostReadGrid = ATP_HOST_READ_GRID;
 constexpr uint64_t kOutboundGrid = 8;
 std::map<std::pair<hipStream_t, hipStream_t>, bool> g_same_queue;  // under g_pool_mu
 
@@ -267,14 +279,14 @@ void check_kernel_host_buffer(const void *p, uint64_t bytes, const char *what) {
   if (!bytes) return;
   if (!p) throw Error(ATP_EINVAL, std::string(what) + " is NULL");
   if (reinterpret_cast<uintptr_t>(p) % 256)
-    throw Error(ATP_EALIGN, std::string(what) + " must be 256-byte aligned for an in-place reshard");
+    throw Error(ATP_EALIGN, std::string(what) + " must be 256-byte aligned (the copy kernel accesses it directly)");
   for (const char *q : {static_cast<const char *>(p), static_cast<const char *>(p) + bytes - 1}) {
     hipPointerAttribute_t a{};
     if (hipPointerGetAttributes(&a, q) != hipSuccess || a.type != hipMemoryTypeHost || a.hostPointer == nullptr ||
         a.devicePointer != a.hostPointer) {
       (void)hipGetLastError();
       throw Error(ATP_EINVAL, std::string(what) +
-                                  " must be pinned host memory from hipHostMalloc for an in-place reshard "
+                                  " must be pinned host memory from hipHostMalloc "
                                   "(the copy kernel accesses it directly)");
     }
   }
@@ -447,9 +459,14 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   int32_t *dev_err = reinterpret_cast<int32_t *>(b_st + c.off_meta);
   int32_t *dev_live = kvcall ? reinterpret_cast<int32_t *>(b_st + c.off_kvlive) : nullptr;
 
-  // the side streams are chosen before this call queues anything: the probe
-  // waits for what the caller's streams already hold
-  if (do_out) choose_side(E, compute, copy);
+  // The side stream runs, in place, the weights call's outbound reads,
+  // levels and host reads and the KV call's outbound copies; out of place,
+  // the host reads of both calls, beside the repack on `compute`.  It is
+  // chosen before this call queues anything: the probe waits for what the
+  // caller's streams already hold.
+  const bool early_reads = !P.inplace && !c.host_reads.empty();
+  const bool use_side = do_out || early_reads;
+  if (use_side) choose_side(E, compute, copy);
 
   // every stream starts after what the caller already queued on `compute`
   // The other call of a weights + KV pair may already be pending: its
@@ -495,6 +512,34 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // k_prepare is the only writer of the error word: it stores it once
   hipLaunchKernelGGL(k_prepare, dim3(1), dim3(1024), 0, compute, pa);
   HIPCHK(hipGetLastError());
+  hipEvent_t prepared = nullptr;  // descriptors, prefix sums and live blocks in place
+  if (use_side) {
+    prepared = E.ev_sync();
+    HIPCHK(hipEventRecord(prepared, compute));
+  }
+
+  // the copy kernel reads inflow pieces from the pinned host buffer into
+  // their final place (kind 4 launches)
+  auto issue_host_reads = [&](hipStream_t s) {
+    for (const Launch &L : c.host_reads) {
+      CallState::LaunchRec r{4, -1, L.bytes, E.ev_time(), E.ev_time()};
+      HIPCHK(hipEventRecord(r.e0, s));
+      launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s,
+                  kHostReadGrid);
+      HIPCHK(hipEventRecord(r.e1, s));
+      cs.launches.push_back(r);
+      cs.h2d_bytes += L.bytes;
+    }
+    cs.hr1 = E.ev_time();
+    HIPCHK(hipEventRecord(cs.hr1, s));
+  };
+  cs.hr1 = nullptr;
+  // out of place: at once, on the side stream, beside the repack (the two
+  // write disjoint bytes of the new arena)
+  if (early_reads) {
+    HIPCHK(hipStreamWaitEvent(E.side, prepared, 0));
+    issue_host_reads(E.side);
+  }
 
   // ---- outbound (in place): read before overwrite ---------------------------------
   // The weights call's outbound reads are copy-kernel launches on the side
@@ -508,9 +553,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   const bool split = do_out && !kvcall;
   hipStream_t late_comp = compute;
   if (split) {
-    late_comp = E.side;
-    hipEvent_t prepared = E.ev_sync();  // the outbound launches read the descriptors
-    HIPCHK(hipEventRecord(prepared, compute));
+    late_comp = E.side;  // the outbound launches read the descriptors
     HIPCHK(hipStreamWaitEvent(late_comp, prepared, 0));
   }
   std::vector<size_t> pos_of(c.outbound.size(), 0);
@@ -588,15 +631,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // in place: the copy kernel reads every gated or strided inflow piece from
   // the pinned host buffer into its final place, after the last level (and,
   // for the weights, after every outbound read)
-  for (const Launch &L : c.host_reads) {
-    CallState::LaunchRec r{4, -1, L.bytes, E.ev_time(), E.ev_time()};
-    HIPCHK(hipEventRecord(r.e0, late_comp));
-    launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, late_comp,
-                kHostReadGrid);
-    HIPCHK(hipEventRecord(r.e1, late_comp));
-    cs.launches.push_back(r);
-    cs.h2d_bytes += L.bytes;
-  }
+  if (P.inplace && !c.host_reads.empty()) issue_host_reads(late_comp);
 
   // KV outbound gathered into staging at level 0: copy it out after that level
   if (do_out && kvcall) {
@@ -639,16 +674,8 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     slot_free[i] = E.ev_sync();
     HIPCHK(hipEventRecord(slot_free[i], late_comp));
   }
-  cs.h2d1 = E.ev_time();
-  if (!c.host_reads.empty()) {
-    // the inflow ends with the later of the copy stream and the host reads
-    hipEvent_t copied = E.ev_sync();
-    HIPCHK(hipEventRecord(copied, copy));
-    HIPCHK(hipStreamWaitEvent(late_comp, copied, 0));
-    HIPCHK(hipEventRecord(cs.h2d1, late_comp));
-  } else {
-    HIPCHK(hipEventRecord(cs.h2d1, copy));
-  }
+  cs.h2d1 = E.ev_time();  // the inflow ends with the later of this and hr1
+  HIPCHK(hipEventRecord(cs.h2d1, copy));
 
   // ---- tails ----------------------------------------------------------------------
   HIPCHK(hipMemcpyAsync(cs.err_host, dev_err, sizeof(int32_t), hipMemcpyDeviceToHost, compute));
@@ -657,7 +684,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   cs.tail_copy = E.ev_sync();
   HIPCHK(hipEventRecord(cs.tail_copy, copy));
   cs.tail_side = nullptr;
-  if (do_out) {
+  if (use_side) {
     // the side stream is not joined back into the caller's streams (that
     // would hold up the other call's work); atp_sync waits for it
     cs.tail_side = E.ev_sync();
@@ -709,7 +736,8 @@ int exec_sync(Plan &P, atp_timing *out) {
     rep_ms += busy;
     // union span of both calls: the earlier start, the later end
     if (cs.h2d0 && (!h2d_first || ms(cs.h2d0, h2d_first) > 0)) h2d_first = cs.h2d0;
-    if (cs.h2d1 && (!h2d_last || ms(h2d_last, cs.h2d1) > 0)) h2d_last = cs.h2d1;
+    for (hipEvent_t e : {cs.h2d1, cs.hr1})
+      if (e && (!h2d_last || ms(h2d_last, e) > 0)) h2d_last = e;
     t.d2h_ms = std::max(t.d2h_ms, ms(cs.d2h0, cs.d2h1));
     for (const auto &L : cs.launches) {
       double m = ms(L.e0, L.e1);

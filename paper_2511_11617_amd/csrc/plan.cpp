@@ -1066,17 +1066,19 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
     return k;
   };
   std::vector<const Pending *> ring;  // through the landing ring
-  std::vector<Fam> host_pieces;       // in place: read by the copy kernel
+  std::vector<Fam> host_pieces;       // read by the copy kernel from the host buffer
   uint64_t ring_total = 0, max_item = 0;
   for (const Pending &pd : inflow) {
-    // Only large contiguous gaps land directly: every copy command costs the
-    // copy engine a fraction of a millisecond, so small gaps travel in large
-    // sequential chunks through the landing ring and a scatter places them.
-    // In place, the weight landings that wait for a level or an outbound
-    // read are read by the copy kernel from the host buffer after the last
-    // level: a copy command that waits holds up every later host-to-device
-    // copy on the DMA engine.  The KV landings go through the ring, whose
-    // copies wait only for their slot's previous scatter.
+    // Only large contiguous gaps land directly on the DMA engine, each copy
+    // command and each event between them costing it tens of microseconds.
+    // Every other piece is read by the copy kernel straight from the pinned
+    // host buffer into its final place: out of place from the start, beside
+    // the repack (the two write disjoint bytes); in place, for the weights,
+    // after the last level, since a copy command that waits for a level or
+    // an outbound read holds up every later host-to-device copy on the DMA
+    // engine.  The in-place KV landings go through the landing ring, whose
+    // copies wait only for their slot's previous scatter and land while the
+    // KV levels run.
     if (pd.contiguous && pd.fam.bytes() >= kDirectMin) {
       HostCopy h;
       h.host_off = pd.host_off;
@@ -1096,21 +1098,22 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
         continue;
       }
     }
-    if (P.inplace && !kvcall) {
+    if (!(P.inplace && kvcall)) {
       Fam f = pd.fam;  // source side: packed host offsets
       f.flags = (f.flags & ~(3u << DF_SRC_SHIFT)) | (BUF_IN << DF_SRC_SHIFT);
       host_pieces.push_back(f);
     } else {
-      // out of place, or the KV call in place: nothing here is read by an
-      // outbound copy (KV outbound is gathered at level 0), and the scatters
-      // run after every level
+      // the KV call in place: nothing here is read by an outbound copy (KV
+      // outbound is gathered at level 0), and the scatters run after every
+      // level
       const Fam &f = pd.fam;
       ring.push_back(&pd);
       ring_total += f.bytes();
       max_item = std::max<uint64_t>(max_item, f.rows * f.run);
     }
   }
-  if (!host_pieces.empty()) emit_group(c, host_pieces, c.n_levels, 4, c.host_reads, live_hint);
+  // level: in place after the last level, out of place at any time (-1)
+  if (!host_pieces.empty()) emit_group(c, host_pieces, P.inplace ? c.n_levels : -1, 4, c.host_reads, live_hint);
 
   uint64_t slot = 0;
   if (!ring.empty()) {

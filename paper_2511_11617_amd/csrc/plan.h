@@ -95,12 +95,13 @@ struct CallPlan {
   std::vector<Chunk> chunks;
   std::vector<HostCopy> outbound;
   std::vector<int> out_order;   // outbound issue order (by the level needing it)
-  // In place, no host-to-device copy command waits long for an event: such
-  // a command holds up every later host-to-device copy of the process on
-  // the DMA engine.  Every weight inflow piece that waits for a level or an
-  // outbound read is read by the copy kernel straight from the pinned
-  // inflow buffer after the call's last level (KV inflow takes the landing
-  // ring, which waits only for its own scatters).  The weights' outbound
+  // Inflow other than large contiguous gaps is read by the copy kernel
+  // straight from the pinned inflow buffer (host_reads): out of place from
+  // the call's start, in place after the call's last level.  In place, no
+  // host-to-device copy command waits long for an event: such a command
+  // holds up every later host-to-device copy of the process on the DMA
+  // engine (the in-place KV inflow takes the landing ring, which waits only
+  // for its own scatters).  The weights' outbound
   // reads are copy-kernel descriptors too (out_d0 + k for position k of
   // out_order), writing straight into the pinned outbound buffer: the
   // runtime's own device-to-host copies are wide blit kernels that starve

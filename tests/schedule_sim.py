@@ -8,7 +8,10 @@ header states, on numpy byte buffers:
     or that two copies write, is reported as a hazard;
   * host inflow landings happen as early as the schedule allows and a later
     level that reads a landed byte is reported; outbound reads happen as
-    late as allowed and must not see bytes an earlier level wrote.
+    late as allowed and must not see bytes an earlier level wrote;
+  * a landing that waits for nothing runs beside the levels, so the bytes
+    it writes must be disjoint from every level's, scatter's and other
+    landing's.
 The replayed arena is then compared with the oracle by the caller.
 """
 from __future__ import annotations
@@ -204,3 +207,16 @@ def replay(cps, bufs: dict, live: np.ndarray):
     land_ready()
     if pending:
         raise Hazard("inflow landing whose gates never open")
+    # a landing that waits for nothing runs beside the levels and scatters:
+    # the bytes it writes must be disjoint from theirs and from each other's
+    for buf in (OLD, NEW):
+        ll = [(d, d + x.run) for x in cps if x.op == H2D and x.level < 0 and x.dst_buf == buf
+              for d in [_lines(x, live)[1]]]
+        if not ll:
+            continue
+        lo, hi = np.concatenate([a for a, _ in ll]), np.concatenate([b for _, b in ll])
+        if not _self_disjoint(lo, hi):
+            raise Hazard("two landings write the same bytes")
+        wl, wh = cat(written[buf])
+        if _overlaps(lo, hi, wl, wh):
+            raise Hazard("a landing and a level or scatter write the same bytes")

@@ -5,6 +5,7 @@ reads bytes it or a sibling overwrites, inflow landing on bytes a later
 level still reads, outbound reads after an overwrite) and wrong addresses,
 before anything runs on a GPU.
 """
+import ctypes as C
 import random
 
 import numpy as np
@@ -16,11 +17,12 @@ from paper_2511_11617_amd import atp, problem
 from synth import configs, pagetable
 from synth.content import KIND_TAG16, Content
 from tests.gpu_harness import CachedContent
-from tests.schedule_sim import INFLOW, NEW, OLD, OUTBOUND, STAGING, copies, replay
+from tests.schedule_sim import (D2H, H2D, INFLOW, NEW, OLD, OUTBOUND, REPACK, STAGING, Copy, Hazard,
+                                 copies, replay)
 from tests.test_oracle_repack import tiny_cfg
 
 
-def sim_case(c, flags=0, staging_cap=0, assign="inorder"):
+def sim_case(c, flags=0, staging_cap=0, assign="inorder", mutate=None):
     pb = model.build(c, assign=assign)
     content = CachedContent(Content(c["seed"], c["w_kind"], c["kv_kind"]))
     table, pool = pagetable.make_for(c)
@@ -41,6 +43,8 @@ def sim_case(c, flags=0, staging_cap=0, assign="inorder"):
     ]
     for which, old, want, mask, inflow, outbound, staging in cases:
         cps = copies(plan, which)
+        if mutate is not None:
+            cps = mutate(which, cps)
         n = max(old.size, want.size)
         bufs = {
             OLD: np.full(n if inplace else old.size, 0xA5, np.uint8),
@@ -92,3 +96,54 @@ def test_large_shapes_one_layer(n, inplace):
 def test_cfg5_shape_in_place_two_layers():
     c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=128, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
     sim_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"])
+
+
+# ---- the replay catches planted schedule mistakes ---------------------------------------
+
+def _clone(x, **kw):
+    y = Copy()
+    C.pointer(y)[0] = x
+    for k, v in kw.items():
+        setattr(y, k, v)
+    return y
+
+
+def _tiny(self_old=0):
+    return configs.get(1, self_old=self_old, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+
+
+def test_replay_catches_a_landing_on_repacked_bytes():
+    # out of place the landings run beside the repack: a landing that writes
+    # bytes a repack copy also writes is a race
+    def plant(which, cps):
+        if which:
+            return cps
+        y = min((x for x in cps if x.op == REPACK), key=lambda x: x.run * x.rows)
+        return cps + [_clone(y, op=H2D, level=-1)]
+    with pytest.raises(Hazard, match="a landing and a level"):
+        sim_case(_tiny(), mutate=plant)
+
+
+def test_replay_catches_two_writers_in_one_level():
+    def plant(which, cps):
+        ys = [x for x in cps if x.op == REPACK and x.level == 1]
+        return cps + [_clone(ys[0])] if ys else cps
+    with pytest.raises(Hazard, match="two copies write the same bytes"):
+        sim_case(_tiny(), flags=atp.INPLACE, mutate=plant)
+
+
+def test_replay_catches_an_outbound_read_after_its_overwrite():
+    def plant(which, cps):
+        return [_clone(x, level=999) if x.op == D2H and x.level >= 1 else x for x in cps]
+    with pytest.raises(Hazard, match="outbound read after an overwrite"):
+        sim_case(_tiny(self_old=2), flags=atp.INPLACE, mutate=plant)
+
+
+def test_replay_catches_an_access_past_a_buffer():
+    def plant(which, cps):
+        if which:
+            return cps
+        y = next(x for x in cps if x.op == REPACK)
+        return [_clone(x, dst_off=x.dst_off + (1 << 40)) if x is y else x for x in cps]
+    with pytest.raises(Hazard, match="access outside buffer"):
+        sim_case(_tiny(), mutate=plant)
