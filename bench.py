@@ -32,7 +32,7 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 # kernel sources hash to `src`.
 COUNTED_TRAFFIC = {
     "src": "d9999845543f9207",
-    "dense-40L-h5120-tp4to3": {"kv": 10738045781, "weights": 9069669589},
+    "dense-40L-h5120-tp4to3": {"kv": 10738016256, "weights": 9069477888},
 }
 
 
