@@ -17,6 +17,7 @@ of a whole step, which the PCIe-bound inflow dominates.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -238,6 +239,8 @@ def main():
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
     recs, launches = [], []
     elapsed = 0.0
+    gc.collect()
+    gc.disable()  # a collector pause is no part of the reshard (one took 45 ms in a step)
     for i in range(args.steps):
         if inplace:
             fill_old()  # restore the old layout (untimed)
@@ -251,6 +254,8 @@ def main():
         log(f"[bench] step {i + 1}/{args.steps}: wall {t.wall_ms:.1f} ms, repack "
             f"{t.repack_union_ms:.3f} ms, h2d {t.h2d_ms:.1f} ms, d2h {t.d2h_ms:.1f} ms, "
             f"issue {issue[-1][0]:.1f} + {issue[-1][1]:.1f} ms")
+
+    gc.enable()
 
     if args.calib_copy_gib > 0:
         n = int(args.calib_copy_gib * (1 << 30))
@@ -485,6 +490,8 @@ def state_main(args):
             step()
             log(f"[state] warmup {i + 1}/{args.warmup} done")
         steps, elapsed = [], 0.0
+        gc.collect()
+        gc.disable()  # a collector pause is no part of the reshard
         for i in range(args.steps):
             torch.cuda.synchronize()
             t1 = time.perf_counter()
@@ -495,6 +502,7 @@ def state_main(args):
             log(f"[state] step {i + 1}/{args.steps}: walls " +
                 " ".join(f"{t.wall_ms:.1f}" for t, _ in recs) + " ms, repack " +
                 f"{sum(t.repack_union_ms for t, _ in recs):.3f} ms")
+        gc.enable()
         for ptr_w, ptr_k in mapped:
             cl.release(ptr_w[0])
             cl.release(ptr_k[0])
