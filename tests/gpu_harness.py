@@ -38,6 +38,21 @@ class CachedContent:
         return self.c(tag, layer, idx)
 
 
+SQUEEZED_RING_CAP = 24 << 20
+
+
+def squeezed_ring_cfg():
+    """A tiny decoder with 4 KV heads (GQA groups of 2), TP 4 -> 3, old rank 2
+    -> new rank 1, whose in-place KV inflow is one head of every live block:
+    64 MiB for 64 sessions of 2048 tokens.  Under SQUEEZED_RING_CAP bytes of
+    staging the landing ring shrinks to 4 slots of 4 MiB that 16 chunks
+    reuse in turn."""
+    from synth import configs
+    from synth.content import KIND_TAG16
+    return configs.get(1, hidden=512, n_q=8, n_kv=4, head_dim=64, new_q_widths=None, new_ffn_widths=None,
+                       self_old=2, n_seq=64, seq_tokens=2048, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+
+
 def say(msg):
     print(msg, flush=True)
     sys.stdout.flush()

@@ -15,7 +15,7 @@ import torch
 from paper_2511_11617_amd import atp
 from synth import configs
 from synth.content import KIND_RAW16, KIND_TAG16
-from tests.gpu_harness import run_case
+from tests.gpu_harness import SQUEEZED_RING_CAP, run_case, squeezed_ring_cfg
 from tests.test_oracle_repack import tiny_cfg
 
 pytestmark = pytest.mark.gpu
@@ -65,6 +65,11 @@ def test_random_small_in_place(seed):
 def test_large_shapes_one_layer(n, inplace):
     c = configs.scaled(n, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
     run_case(c, flags=atp.INPLACE if inplace else 0, name=f"cfg{n}-1layer" + ("-inplace" if inplace else ""))
+
+
+def test_in_place_ring_under_a_squeezed_staging_cap():
+    c = squeezed_ring_cfg()
+    run_case(c, flags=atp.INPLACE, staging_cap=SQUEEZED_RING_CAP, name="ring-squeezed-inplace")
 
 
 def test_cfg5_shape_in_place_two_layers():

@@ -16,7 +16,7 @@ from oracle import model, repack
 from paper_2511_11617_amd import atp, problem
 from synth import configs, pagetable
 from synth.content import KIND_TAG16, Content
-from tests.gpu_harness import CachedContent
+from tests.gpu_harness import SQUEEZED_RING_CAP, CachedContent, squeezed_ring_cfg
 from tests.schedule_sim import (D2H, H2D, INFLOW, NEW, OLD, OUTBOUND, REPACK, STAGING, Copy, Hazard,
                                  copies, replay)
 from tests.test_oracle_repack import tiny_cfg
@@ -96,6 +96,14 @@ def test_large_shapes_one_layer(n, inplace):
 def test_cfg5_shape_in_place_two_layers():
     c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=128, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
     sim_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"])
+
+
+def test_in_place_ring_under_a_squeezed_staging_cap():
+    c = squeezed_ring_cfg()
+    plan = sim_case(c, flags=atp.INPLACE, staging_cap=SQUEEZED_RING_CAP)
+    st_ = plan.stats()
+    # the ring shrank to fit: far less staging than the KV inflow it carries
+    assert st_.staging_kv <= SQUEEZED_RING_CAP and st_.staging_kv * 3 < st_.inflow_kv
 
 
 # ---- the replay catches planted schedule mistakes ---------------------------------------
