@@ -39,6 +39,15 @@ def test_cfg1_eviction_ids_kept(flags):
     run_case(c, flags=flags, evict=(last, 0.5), name=f"cfg1-evict-flags{flags}")
 
 
+@pytest.mark.parametrize("flags", [atp.KV_COMPACT, 0, atp.INPLACE])
+def test_cfg1_zero_budget_evicts_every_session(flags):
+    """No live block is left: the KV call moves and lands nothing, and the
+    weights are resharded as usual."""
+    c = configs.get(1, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    last = np.random.default_rng(7).permutation(c["n_seq"])
+    run_case(c, flags=flags, evict=(last, 0.0), name=f"cfg1-evict-all-flags{flags}")
+
+
 @pytest.mark.parametrize("seed", [2, 11, 40])
 def test_tiny_compact_after_eviction(seed):
     c = tiny_cfg(random.Random(seed), experts=seed % 2 == 1)

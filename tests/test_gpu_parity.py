@@ -17,6 +17,7 @@ from synth import configs
 from synth.content import KIND_RAW16, KIND_TAG16
 from tests.gpu_harness import SQUEEZED_RING_CAP, run_case, squeezed_ring_cfg
 from tests.test_oracle_repack import tiny_cfg
+from tests.test_schedule_sim import single_target_cfg
 
 pytestmark = pytest.mark.gpu
 
@@ -65,6 +66,12 @@ def test_random_small_in_place(seed):
 def test_large_shapes_one_layer(n, inplace):
     c = configs.scaled(n, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
     run_case(c, flags=atp.INPLACE if inplace else 0, name=f"cfg{n}-1layer" + ("-inplace" if inplace else ""))
+
+
+@pytest.mark.parametrize("self_old,inplace", [(0, False), (0, True), (1, False), (1, True)])
+def test_single_target_takes_every_tensor_whole(self_old, inplace):
+    run_case(single_target_cfg(self_old), flags=atp.INPLACE if inplace else 0,
+             name=f"tp2to1-self{self_old}" + ("-inplace" if inplace else ""))
 
 
 def test_in_place_ring_under_a_squeezed_staging_cap():

@@ -98,6 +98,33 @@ def test_cfg5_shape_in_place_two_layers():
     sim_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"])
 
 
+def single_target_cfg(self_old):
+    """TP 2 -> 1: the survivor ends up holding every tensor whole."""
+    return configs.get(1, old_tp=2, new_tp=1, failed=[1 - self_old], self_old=self_old, new_q_widths=None,
+                       new_ffn_widths=None, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+
+
+@pytest.mark.parametrize("self_old,inplace", [(0, False), (0, True), (1, False), (1, True)])
+def test_single_target_takes_every_tensor_whole(self_old, inplace):
+    plan = sim_case(single_target_cfg(self_old), flags=atp.INPLACE if inplace else 0)
+    st_ = plan.stats()
+    assert st_.self_new_rank == 0 and st_.global_reload == st_.reload_min
+    assert st_.retained_w + st_.inflow_w == st_.new_arena_bytes  # shards are 256-aligned, none padded here
+
+
+def test_no_live_kv_block_plans_no_kv_copy():
+    c = configs.get(1)
+    table, pool = pagetable.make_for(c)
+    n_live = len(repack.live_blocks(table))
+    for flags in (0, atp.INPLACE, atp.KV_COMPACT):
+        plan = problem.build(c, n_live=0, pool=pool, flags=flags).plan()
+        st_ = plan.stats()
+        assert copies(plan, 1) == [] and st_.inflow_kv == st_.retained_kv == st_.moved_kv == 0
+        # by id the arena keeps every block's place; compact, it holds no block
+        full = problem.build(c, n_live=n_live, pool=pool, flags=flags).plan().stats().new_kv_bytes
+        assert st_.new_kv_bytes == (0 if flags & atp.KV_COMPACT else full) and full > 0
+
+
 def test_in_place_ring_under_a_squeezed_staging_cap():
     c = squeezed_ring_cfg()
     plan = sim_case(c, flags=atp.INPLACE, staging_cap=SQUEEZED_RING_CAP)
