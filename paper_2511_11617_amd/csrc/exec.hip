@@ -174,8 +174,11 @@ __global__ void k_spin(uint32_t iters) {
 }
 __global__ void k_nop() {}
 
-constexpr uint32_t kSpinIters = 400;     // about 1.4 ms at 2.4 GHz
-constexpr float kSpinMarginMs = 0.3f;    // the empty kernel must finish this much earlier
+// The probe sits on the first reshard of a process (per caller stream pair),
+// so it is kept short: on another queue the empty kernel ends within
+// microseconds of its launch, on the same queue only after the spin.
+constexpr uint32_t kSpinIters = 100;     // about 0.34 ms at 2.4 GHz
+constexpr float kSpinMarginMs = 0.15f;   // the empty kernel must finish this much earlier
 
 // Workgroups of the launches that move bytes over PCIe with the copy kernel
 // (persistent grids over their tiles).  Host reads: 32 workgroups carry a
