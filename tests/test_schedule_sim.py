@@ -84,6 +84,28 @@ def test_random_small(seed, experts, inplace):
     sim_case(c, flags=atp.INPLACE if inplace else 0)
 
 
+@settings(max_examples=40, deadline=None)
+@given(st.integers(0, 2 ** 31), st.booleans())
+def test_random_small_in_place_under_a_staging_cap(seed, experts):
+    """A cap at the unconstrained staging need is accepted; one below it is
+    either refused with ATP_ECAPACITY or met by a plan that still replays
+    to the oracle's bytes."""
+    c = tiny_cfg(random.Random(seed), experts)
+    table, pool = pagetable.make_for(c)
+    n_live = len(repack.live_blocks(table))
+    free = problem.build(c, n_live=n_live, pool=pool, flags=atp.INPLACE).plan().stats()
+    need = max(free.staging_w, free.staging_kv)
+    plan = sim_case(c, flags=atp.INPLACE, staging_cap=need)
+    assert max(plan.stats().staging_w, plan.stats().staging_kv) <= need
+    try:
+        tight = problem.build(c, n_live=n_live, pool=pool, flags=atp.INPLACE, staging_cap=need - 256).plan()
+    except atp.AtpError as e:
+        assert e.code == atp.ECAPACITY
+        return
+    assert max(tight.stats().staging_w, tight.stats().staging_kv) <= need - 256
+    sim_case(c, flags=atp.INPLACE, staging_cap=need - 256)
+
+
 @pytest.mark.slow
 @pytest.mark.parametrize("inplace", [False, True])
 @pytest.mark.parametrize("n", [2, 3, 4])
