@@ -651,9 +651,11 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   }
 
   // ---- inflow ------------------------------------------------------------------------
-  // (direct landings went first, none of them waits for anything)
-  // ring: H2D into a slot, then a scatter from it after every level; a chunk
-  // reuses its slot once the slot's previous scatter is done
+  // (direct landings went first, none of them waits for anything; the copy
+  // kernel's host reads are issued above)
+  // ring (the in-place KV call only): H2D into a slot, then a scatter from it
+  // after every level; a chunk reuses its slot once the slot's previous
+  // scatter is done
   std::vector<hipEvent_t> slot_free(c.chunks.size(), nullptr);
   for (size_t i = 0; i < c.chunks.size(); ++i) {
     const Chunk &ch = c.chunks[i];
