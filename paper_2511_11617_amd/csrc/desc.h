@@ -29,6 +29,7 @@ enum : uint32_t {
                           // kernel rewrites them as live-list positions
   DF_ALIGNED = 1u << 7,   // every offset, pitch, stride and run is a
                           // multiple of 16: the 16-byte vector kernel
+  DF_WIDE = 1u << 8,      // aligned, tiled kWideUnroll chunks per thread
 };
 
 // Launch shape of the vector kernel: 256 threads, ATP_UNROLL independent
@@ -52,6 +53,15 @@ enum : uint32_t {
 constexpr int kThreads = 256;
 constexpr int kUnroll = ATP_UNROLL;
 constexpr int64_t kTileChunks = kThreads * kUnroll;
+// Short aligned KV lines (a head of one block, 4 KiB or less) take tiles
+// twice as wide, which keeps more bytes in flight per thread: the largest KV
+// level of the 80-layer TP 8->7 reshard ran 5 % faster so, while the
+// weights' long lines ran slower.
+constexpr int kWideUnroll = 2 * ATP_UNROLL;
+constexpr int64_t kWideTileChunks = kThreads * kWideUnroll;
+constexpr uint64_t kWideMaxRun = 4096;
+// 16-byte chunks per tile of a vector-kernel descriptor
+constexpr int64_t tile_chunks(uint32_t flags) { return (flags & DF_WIDE) ? kWideTileChunks : kTileChunks; }
 // bytes per tile of the 2-byte-granular (LDS funnel-shift) kernel
 constexpr int64_t kSegBytes = 8192;
 

@@ -370,6 +370,23 @@ void check_extents(const CallPlan &c, bool kvcall, const Plan &P, uint64_t in_by
     uint64_t lines = uint64_t(kvcall ? std::max<int64_t>(nb, f.o_end - f.o_begin) : f.o_end - f.o_begin) * f.rows;
     if (lines * (f.run / 16 + 1) >= (uint64_t(1) << 32)) throw Error(ATP_EINVAL, "copy family too large");
   }
+  // a launch's kernel tiles its descriptors the way the prepare kernel
+  // counted them: the flags of every descriptor must match the launch
+  auto same_shape = [&](const Launch &L) {
+    for (int d = L.d0; d < L.d1; ++d) {
+      const uint32_t fl = c.fams[size_t(d)].flags;
+      if (((fl & DF_ALIGNED) != 0) != L.aligned || ((fl & DF_WIDE) != 0) != (L.aligned && L.wide))
+        throw Error(ATP_EINVAL, "internal: a launch mixes descriptor shapes");
+    }
+  };
+  for (const Launch &L : c.levels) same_shape(L);
+  for (const Launch &L : c.host_reads) same_shape(L);
+  for (const Chunk &ch : c.chunks)
+    for (const Launch &L : ch.scatters) same_shape(L);
+  for (size_t k = 0; k < c.out_aligned.size(); ++k)
+    if (((c.fams[size_t(c.out_d0) + k].flags & DF_ALIGNED) != 0) != (c.out_aligned[k] != 0) ||
+        (c.fams[size_t(c.out_d0) + k].flags & DF_WIDE))
+      throw Error(ATP_EINVAL, "internal: an outbound read has the wrong shape");
 }
 
 void launch_copy(Exec &E, const Launch &L, const Desc *dev_desc, const int64_t *dev_prefix, char *b0, char *b1,
@@ -378,9 +395,12 @@ void launch_copy(Exec &E, const Launch &L, const Desc *dev_desc, const int64_t *
   // over the tiles of the launch)
   uint64_t cap = grid_cap ? grid_cap : ATP_PERSIST ? uint64_t(E.grid_max) : (uint64_t(1) << 30);
   uint64_t g = std::min<uint64_t>(std::max<uint64_t>(L.tiles_max, 1), cap);
-  if (L.aligned)
-    hipLaunchKernelGGL(k_copy16, dim3(unsigned(g)), dim3(kThreads), 0, s, dev_desc, dev_prefix, L.d0, L.d1, b0, b1,
-                       b2, live);
+  if (L.aligned && L.wide)
+    hipLaunchKernelGGL((k_copy16<kWideUnroll>), dim3(unsigned(g)), dim3(kThreads), 0, s, dev_desc, dev_prefix, L.d0,
+                       L.d1, b0, b1, b2, live);
+  else if (L.aligned)
+    hipLaunchKernelGGL((k_copy16<kUnroll>), dim3(unsigned(g)), dim3(kThreads), 0, s, dev_desc, dev_prefix, L.d0,
+                       L.d1, b0, b1, b2, live);
   else
     hipLaunchKernelGGL(k_copy_bytes, dim3(unsigned(g)), dim3(kThreads), 0, s, dev_desc, dev_prefix, L.d0, L.d1, b0,
                        b1, b2, live);

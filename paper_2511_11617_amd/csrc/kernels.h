@@ -134,7 +134,7 @@ __global__ void __launch_bounds__(1024) k_prepare(PrepArgs a) {
     uint64_t lines = uint64_t(x.o_end - x.o_begin) * x.rows;
     uint64_t tiles;
     if (x.flags & DF_ALIGNED)
-      tiles = (lines * (x.run >> 4) + kTileChunks - 1) / kTileChunks;
+      tiles = (lines * (x.run >> 4) + tile_chunks(x.flags) - 1) / tile_chunks(x.flags);
     else
       tiles = lines * ((x.run + kSegBytes - 1) / kSegBytes);
     a.prefix[d] = int64_t(tiles);  // temporarily the count
@@ -235,19 +235,23 @@ __device__ __forceinline__ int64_t tile_of_block() {
 // that no load waits behind another's address computation.  Lanes past the
 // end of the tile load its last chunk again (a valid address) and store
 // nothing: unconditional loads keep the compiler from waiting on each one.
+// U chunks per thread: every descriptor of a launch has DF_WIDE exactly when
+// U == kWideUnroll (the prepare kernel counted its tiles that way).
+template <int U>
 __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ descs, const int64_t *__restrict__ prefix,
                                                      int d0, int d1, char *b0, char *b1, char *b2,
                                                      const int32_t *__restrict__ live) {
+  constexpr int64_t kTile = int64_t(kThreads) * U;
   const int64_t T0 = prefix[d0], T1 = prefix[d1];
   for (int64_t t = T0 + tile_of_block(); t < T1; t += gridDim.x) {
     const int d = find_desc(prefix, d0, d1, t);
     const Desc x = descs[d];
     const uint32_t cpl = x.run >> 4;
     const uint64_t total = uint64_t(x.o_end - x.o_begin) * x.rows * cpl;
-    const uint64_t cbase = uint64_t(t - prefix[d]) * kTileChunks;
-    const uint64_t clast = (cbase + kTileChunks < total ? cbase + kTileChunks : total) - 1;
+    const uint64_t cbase = uint64_t(t - prefix[d]) * kTile;
+    const uint64_t clast = (cbase + kTile < total ? cbase + kTile : total) - 1;
     const uint32_t l0 = divq(uint32_t(cbase), x.magic_line);
-    u32x4 v[kUnroll];
+    u32x4 v[U];
     if (l0 == divq(uint32_t(clast), x.magic_line)) {
       // the whole tile lies in one line: one address computation per tile
       const LineAddr la = line_addr<true>(x, l0, b0, b1, b2, live);
@@ -256,12 +260,12 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
       const u32x4 *s = reinterpret_cast<const u32x4 *>(la.src) + col0;
       u32x4 *dd = reinterpret_cast<u32x4 *>(la.dst) + col0;
 #pragma unroll
-      for (int k = 0; k < kUnroll; ++k) {
+      for (int k = 0; k < U; ++k) {
         const uint32_t i = threadIdx.x + k * kThreads;
         v[k] = load16(s + (i < n ? i : n - 1));
       }
 #pragma unroll
-      for (int k = 0; k < kUnroll; ++k) {
+      for (int k = 0; k < U; ++k) {
         const uint32_t i = threadIdx.x + k * kThreads;
         if (i < n) store16(dd + i, v[k]);
       }
@@ -269,11 +273,11 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
     }
     // several lines per tile: resolve the line once per wavefront when its
     // 64 chunks share one (short KV head runs), else per lane
-    const u32x4 *sp[kUnroll];
-    u32x4 *dp[kUnroll];
+    const u32x4 *sp[U];
+    u32x4 *dp[U];
     const uint32_t wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
+    for (int k = 0; k < U; ++k) {
       const uint64_t g0r = cbase + uint64_t(k) * kThreads + wv * 64;
       const uint64_t g0 = g0r < clast ? g0r : clast;
       const uint64_t gl = g0r + 63 < clast ? g0r + 63 : clast;
@@ -294,9 +298,9 @@ __global__ void __launch_bounds__(kThreads) k_copy16(const Desc *__restrict__ de
       }
     }
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) v[k] = load16(sp[k]);
+    for (int k = 0; k < U; ++k) v[k] = load16(sp[k]);
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
+    for (int k = 0; k < U; ++k)
       if (cbase + threadIdx.x + uint64_t(k) * kThreads <= clast) store16(dp[k], v[k]);
   }
 }

@@ -715,29 +715,38 @@ bool fam_aligned(const Fam &f) {
          f.dst_pitch % 16 == 0 && f.src_ostride % 16 == 0 && f.dst_ostride % 16 == 0;
 }
 
+// Tiles of a family whose DF_ALIGNED / DF_WIDE flags are set.
 uint64_t fam_tiles(const Fam &f, int64_t items_hint) {
   uint64_t lines = uint64_t(items_hint) * f.rows;
-  if (fam_aligned(f)) {
+  if (f.flags & DF_ALIGNED) {
     uint64_t chunks = lines * (f.run / 16);
-    return (chunks + kTileChunks - 1) / kTileChunks;
+    return (chunks + uint64_t(tile_chunks(f.flags)) - 1) / uint64_t(tile_chunks(f.flags));
   }
   return lines * ((f.run + kSegBytes - 1) / kSegBytes);
 }
 
-// Emit launches for a group of families: aligned ones first, then the
-// 2-byte-granular ones.  Families are appended to c.fams.
+// Emit launches for a group of families: aligned ones first (with wide
+// tiles, if `allow_wide`, for short KV lines), then the 2-byte-granular ones.
+// Families are appended to c.fams; every family of a launch has the same
+// DF_ALIGNED and DF_WIDE flags.
 void emit_group(CallPlan &c, std::vector<Fam> group, int level, int kind, std::vector<Launch> &out,
-                int64_t live_hint) {
-  for (int pass = 0; pass < 2; ++pass) {
+                int64_t live_hint, bool allow_wide) {
+  for (Fam &f : group) {
+    f.flags &= ~(DF_ALIGNED | DF_WIDE);
+    if (!fam_aligned(f)) continue;
+    f.flags |= DF_ALIGNED;
+    if (allow_wide && f.run <= kWideMaxRun && (f.flags & (DF_SRC_IND | DF_DST_IND | DF_BLOCKRANGE)))
+      f.flags |= DF_WIDE;
+  }
+  for (int pass = 0; pass < 3; ++pass) {
     Launch L;
     L.level = level;
     L.kind = kind;
-    L.aligned = pass == 0;
+    L.aligned = pass < 2;
+    L.wide = pass == 1;
     L.d0 = int(c.fams.size());
-    for (Fam &f : group) {
-      bool al = fam_aligned(f);
-      if (al != L.aligned) continue;
-      if (al) f.flags |= DF_ALIGNED;
+    for (const Fam &f : group) {
+      if (((f.flags & DF_ALIGNED) != 0) != L.aligned || ((f.flags & DF_WIDE) != 0) != L.wide) continue;
       int64_t items = (f.flags & DF_BLOCKRANGE) ? std::min<int64_t>(f.o_end - f.o_begin, live_hint)
                                                 : f.o_end - f.o_begin;
       L.bytes += uint64_t(items) * f.rows * f.run;
@@ -981,7 +990,7 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
   }
   for (int l = 0; l < c.n_levels; ++l) {
     size_t before = c.levels.size();
-    emit_group(c, per_level[l], l, 0, c.levels, live_hint);
+    emit_group(c, per_level[l], l, 0, c.levels, live_hint, true);
     if (P.inplace && !kvcall && c.levels.size() > before) {
       for (size_t o = 0; o < outbound.size(); ++o)
         if (needed_by[o] == l) c.levels[before].wait_outbound.push_back(int(o));
@@ -1113,7 +1122,10 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
     }
   }
   // level: in place after the last level, out of place at any time (-1)
-  if (!host_pieces.empty()) emit_group(c, host_pieces, P.inplace ? c.n_levels : -1, 4, c.host_reads, live_hint);
+  // host reads keep the narrow tile: more bytes in flight over PCIe would
+  // slow the repack beside them
+  if (!host_pieces.empty())
+    emit_group(c, host_pieces, P.inplace ? c.n_levels : -1, 4, c.host_reads, live_hint, false);
 
   uint64_t slot = 0;
   if (!ring.empty()) {
@@ -1142,7 +1154,7 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
       if (pieces.empty()) return;
       ch.slot = next_slot;
       next_slot = (next_slot + 1) % c.n_slots;
-      emit_group(c, pieces, -1, 2, ch.scatters, live_hint);
+      emit_group(c, pieces, -1, 2, ch.scatters, live_hint, true);
       c.chunks.push_back(ch);
       pieces.clear();
       ch = Chunk();

@@ -59,6 +59,7 @@ struct Launch {
   int level = 0;
   int kind = 0;        // 0 repack, 2 scatter, 3 outbound read, 4 host read
   bool aligned = true;
+  bool wide = false;   // aligned, with tiles of kWideTileChunks (DF_WIDE)
   int d0 = 0, d1 = 0;
   uint64_t bytes = 0;  // bytes copied (upper bound for block ranges)
   uint64_t tiles_max = 0;
