@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 # counters read for a plain 4 GiB copy: x2.0 and x1.0), valid only while the
 # kernel sources hash to `src`.
 COUNTED_TRAFFIC = {
-    "src": "d9999845543f9207",
-    "dense-40L-h5120-tp4to3": {"kv": 10738016256, "weights": 9069477888},
+    "src": "98de88c3866af8ac",
+    "dense-40L-h5120-tp4to3": {"kv": 10738028373, "weights": 9069458016},
 }
 
 
