@@ -227,6 +227,18 @@ typedef struct {
  * `out` may be NULL. */
 int atp_sync(atp_plan_t *plan, atp_timing *out);
 
+/* Optional: do, before the first reshard on the current device, the
+ * per-process set-up that reshard would otherwise pay (about 5 ms on the
+ * 40-layer TP 4->3 workload): load the kernels, choose the library's side
+ * stream for this (compute, copy) pair (a probe that waits for what those
+ * streams already hold), and create `events` pooled HIP events of each kind
+ * (0..4096; 256 covers the workloads here) and pinned descriptor buffers.
+ * A process that may have to recover calls it ahead of time, e.g. right
+ * after mapping the state plane's regions.  Calling it again is harmless.
+ * Errors: ATP_EINVAL for `events` out of range, ATP_EHIP without a usable
+ * device. */
+int atp_warmup(atp_stream compute, atp_stream copy, int32_t events);
+
 /* ---- inspection helpers (tests, benchmark) ------------------------------ */
 typedef struct {
   int32_t self_new_rank;

@@ -37,7 +37,7 @@ EXPORTS = [
     "atp_last_error", "atp_st_open", "atp_st_close", "atp_st_find", "atp_load_weights",
     "atp_kv_evict_lru", "atp_daemon_serve", "atp_state_connect", "atp_state_disconnect",
     "atp_state_alloc", "atp_state_open", "atp_state_release", "atp_state_free", "atp_state_put",
-    "atp_state_get", "atp_state_list", "atp_state_shutdown",
+    "atp_state_get", "atp_state_list", "atp_state_shutdown", "atp_warmup",
 ]
 
 
@@ -154,6 +154,7 @@ def _load():
     lib.atp_reshard_kv.argtypes = [P, P, C.c_uint64, P, C.c_uint64, P, C.c_int32, C.c_int32, P,
                                    C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, P]
     lib.atp_sync.argtypes = [P, C.POINTER(Timing)]
+    lib.atp_warmup.argtypes = [P, P, C.c_int32]
     lib.atp_plan_stats.argtypes = [P, C.POINTER(Stats)]
     lib.atp_plan_tasks.argtypes = [P, C.c_int32, C.POINTER(Task), C.c_int32, C.POINTER(C.c_int32)]
     lib.atp_plan_ranges.argtypes = [P, C.c_int32, C.POINTER(Range), C.c_int32, C.POINTER(C.c_int32)]
@@ -217,6 +218,13 @@ def _list(fn, plan, typ, *args):
     arr = (typ * max(n.value, 1))()
     _check(fn(plan, *args, arr, n.value, C.byref(n)))
     return list(arr[:n.value])
+
+
+def warmup(compute: int, copy: int, events: int = 256) -> None:
+    """atp_warmup on the current device: the first reshard's one-time set-up
+    (kernels loaded, side stream chosen for these raw stream handles, pooled
+    events and pinned buffers) done ahead of time."""
+    _check(lib.atp_warmup(compute, copy, events))
 
 
 class Plan:

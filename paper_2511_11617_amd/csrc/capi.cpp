@@ -116,6 +116,13 @@ int atp_sync(atp_plan_t *plan, atp_timing *out) {
   });
 }
 
+int atp_warmup(atp_stream compute, atp_stream copy, int32_t events) {
+  return guard([&]() -> int {
+    atp::exec_warmup(compute, copy, events);
+    return ATP_OK;
+  });
+}
+
 int atp_plan_stats(const atp_plan_t *plan, atp_stats *out) {
   if (!plan || !out) return fail(ATP_EINVAL, "NULL argument");
   *out = plan->p->stats;

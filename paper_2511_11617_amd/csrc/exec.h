@@ -16,5 +16,6 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
 int exec_sync(Plan &P, atp_timing *out);
 void exec_free(Plan &P);
 void exec_launches(const Plan &P, std::vector<atp_launch> &out);
+void exec_warmup(void *compute, void *copy, int events);
 
 }  // namespace atp

@@ -102,3 +102,15 @@ def test_planning_is_deterministic():
     sa, sb = a.stats(), b.stats()
     for f, _ in atp.Stats._fields_:
         assert getattr(sa, f) == getattr(sb, f), f
+
+
+def test_warmup_without_a_gpu_and_with_a_bad_count():
+    with pytest.raises(atp.AtpError) as e:
+        atp.warmup(0, 0, 5000)
+    assert e.value.code == atp.EINVAL
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("this machine has a GPU: the GPU tests cover atp_warmup")
+    with pytest.raises(atp.AtpError) as e:
+        atp.warmup(0, 0)
+    assert e.value.code == atp.EHIP

@@ -188,3 +188,14 @@ def test_fresh_in_place_plans_in_a_row():
         t, plan, st = run_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"], name=f"fresh-in-place-{i}")
         assert st.outbound_w > 0 and t.d2h_bytes == st.outbound_w + st.outbound_kv
         alive.append(plan)
+
+
+def test_warmup_then_reshard():
+    """atp_warmup ahead of the first reshard (twice: harmless), on the streams
+    the reshard then uses; the reshard stays bit-exact."""
+    s0, s1 = torch.cuda.current_stream(), torch.cuda.Stream()
+    atp.warmup(s0.cuda_stream, s1.cuda_stream, 64)
+    atp.warmup(s0.cuda_stream, s1.cuda_stream, 0)
+    torch.cuda.synchronize()
+    for flags in (0, atp.INPLACE):
+        run_case(configs.get(1), flags=flags, name=f"after-warmup-flags{flags}")
