@@ -569,9 +569,9 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // stream that write straight into the pinned outbound buffer, in the
   // plan's order (by the first level that overwrites them), each level right
   // after the reads it needs; pos_ev[k] fires when the first k + 1 have
-  // finished (pos_ev.size() is the number of pieces issued).  That work and the weight inflow read after it stay off the
-  // caller's streams, so that they do not hold up the other call's work
-  // queued behind them.
+  // finished (pos_ev.size() is the number of pieces issued).  That work and
+  // the weight inflow read after it stay off the caller's streams, so that
+  // they do not hold up the other call's work queued behind them.
   std::vector<hipEvent_t> pos_ev;
   const bool split = do_out && !kvcall;
   hipStream_t late_comp = compute;
