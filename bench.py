@@ -66,8 +66,9 @@ def parse():
                          "recency) are evicted least recently used first (atp_kv_evict_lru); out of "
                          "place the kept blocks land in a compact arena (ATP_KV_COMPACT)")
     ap.add_argument("--load", action="store_true",
-                    help="also time the range-read reload source (atp_load_weights) on a checkpoint "
-                         "written for this workload")
+                    help="also time the range-read reload source on a checkpoint written for this "
+                         "workload: the reads alone (atp_load_weights), and reads and reshard pipelined "
+                         "(atp_load_reshard_weights)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the CPU oracle over the whole workload for at least this long")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
@@ -345,7 +346,32 @@ def main():
     if evict is not None:
         out["kv_evict"] = evict
     if args.load:
-        out["load"] = load_leg(args.steps, cfg, plan, st, tl, hin_w, Pinned)
+        def pipelined_step(files, names, buf):
+            """One step whose weight inflow is read from the checkpoint while the
+            weights reshard runs behind the reads (atp_load_reshard_weights)."""
+            if inplace:
+                fill_old()
+            p = built.plan()
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+
+            def kv():
+                p.reshard_kv(ptr(ak), ak.numel(), ptr(nk), nk.numel() if nk is not None else 0,
+                             ptr(table_d), table.shape[0], table.shape[1], ptr(hin_k), st.inflow_kv,
+                             ptr(hout_k), st.outbound_kv if inplace else 0, ptr(stage_k), stage_k.numel(),
+                             compute.cuda_stream, copy.cuda_stream)
+            if not inplace:  # out of place the KV inflow can use the link while the weights are read
+                kv()
+            p.load_reshard_weights(files, names, ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0,
+                                   buf.ptr, st.inflow_w, ptr(hout_w), st.outbound_w if inplace else 0,
+                                   ptr(stage_w), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
+            if inplace:  # in place the weights call comes first
+                kv()
+            p.sync()
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t1) * 1e3
+
+        out["load"] = load_leg(args.steps, cfg, plan, st, tl, hin_w, Pinned, pipelined_step, wall_ms)
     if not args.no_cpu_baseline and evict is None:  # the oracle's leg runs the by-id layout
         if inplace:
             fill_old()
@@ -594,7 +620,7 @@ def state_main(args):
     print(json.dumps(out), flush=True)
 
 
-def load_leg(steps, cfg, plan, st, tl, hin_w, Pinned):
+def load_leg(steps, cfg, plan, st, tl, hin_w, Pinned, pipelined_step, step_ms):
     """Range-read reload source (atp_load_weights).  The checkpoint has the
     headers of every full weight tensor; as data it holds the intervals this
     plan reads, taken from the synthetic inflow, and holes elsewhere (the full
@@ -642,16 +668,32 @@ def load_leg(steps, cfg, plan, st, tl, hin_w, Pinned):
                 ms.append(ls.read_ms)
         if not np.array_equal(buf.tensor.numpy(), src):
             raise RuntimeError("range reads returned other bytes than the checkpoint holds")
+        # reads and reshard together: the file reads overlap the landings
+        pipe = []
+        gc.collect()
+        gc.disable()
+        for i in range(steps + 1):  # the first pass is a warm-up
+            buf.tensor.fill_(0xA5)
+            w = pipelined_step(files, names, buf)
+            if i:
+                pipe.append(w)
+            log(f"[bench] reads + reshard pipelined: {w:.1f} ms")
+        gc.enable()
+        if not np.array_equal(buf.tensor.numpy(), src):
+            raise RuntimeError("pipelined range reads returned other bytes than the checkpoint holds")
         files.close()
         buf.close()
     finally:
         shutil.rmtree(d, ignore_errors=True)
     read_ms = sum(ms) / len(ms)
+    pipe_ms = sum(pipe) / len(pipe)
     return {"source": f"safetensors range reads, file in {where[0]} (page cache)", "bytes": int(st.inflow_w),
             "tensor_bytes": int(ls.tensor_bytes), "read_fraction": round(st.inflow_w / ls.tensor_bytes, 4),
             "reads": int(ls.reads), "threads": int(ls.threads), "read_ms": round(read_ms, 3),
             "GBps": round(st.inflow_w / (read_ms * 1e-3) / 1e9, 2), "file_bytes": int(total),
-            "write_s": round(write_s, 2)}
+            "write_s": round(write_s, 2),
+            "sequential_ms": round(read_ms + step_ms, 3),  # reads, then the step from pinned memory
+            "pipelined_ms": round(pipe_ms, 3)}  # reads and reshard together, whole step
 
 
 def h2d_probe(torch, bufs, max_bytes, stream, chunk=64 << 20):

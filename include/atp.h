@@ -396,6 +396,27 @@ int atp_load_weights(const atp_plan_t *plan, const atp_st_t *st, const char *con
                      int32_t n_names, void *inflow_host, uint64_t inflow_bytes,
                      int32_t n_threads, atp_load_stats *stats);
 
+/* The range-read reload pipelined with the weights reshard (Sec. III-C:
+ * reloads overlapped with the rest of the recovery).  Runs the reads of
+ * atp_load_weights on `n_threads` host threads (0: up to 16) into
+ * inflow_host and enqueues the reshard of atp_reshard_weights (same
+ * arguments and buffer rules), issuing each inflow piece only once the reads
+ * under it have completed, so that the file reads overlap the landings; the
+ * GPU never waits for the host.  Returns once every read is done and all the
+ * work is enqueued; atp_sync as after atp_reshard_weights.  Out of place,
+ * issue atp_reshard_kv first: its inflow then uses the link while the
+ * weights are read.  Name or shape errors are ATP_EINVAL before anything
+ * starts.  A failed read is ATP_EINVAL after the enqueued work has drained
+ * (the plan is then not pending). */
+int atp_load_reshard_weights(atp_plan_t *plan, const atp_st_t *st, const char *const *names,
+                             int32_t n_names, void *arena, uint64_t arena_bytes,
+                             void *new_arena, uint64_t new_arena_bytes,
+                             void *inflow_host, uint64_t inflow_bytes,
+                             void *outbound_host, uint64_t outbound_bytes,
+                             void *staging, uint64_t staging_bytes,
+                             atp_stream compute, atp_stream copy, int32_t n_threads,
+                             atp_load_stats *stats);
+
 /* ---- KV budget under recovery (Sec. III-A: per-session recency; cold KV
  * released least recently used first when the demand exceeds the budget,
  * evicted sessions being rebuilt later by replay) ----------------------- */

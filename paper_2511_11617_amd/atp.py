@@ -37,7 +37,7 @@ EXPORTS = [
     "atp_last_error", "atp_st_open", "atp_st_close", "atp_st_find", "atp_load_weights",
     "atp_kv_evict_lru", "atp_daemon_serve", "atp_state_connect", "atp_state_disconnect",
     "atp_state_alloc", "atp_state_open", "atp_state_release", "atp_state_free", "atp_state_put",
-    "atp_state_get", "atp_state_list", "atp_state_shutdown", "atp_warmup",
+    "atp_state_get", "atp_state_list", "atp_state_shutdown", "atp_warmup", "atp_load_reshard_weights",
 ]
 
 
@@ -170,6 +170,9 @@ def _load():
     lib.atp_st_find.argtypes = [P, C.c_char_p, C.POINTER(StTensor)]
     lib.atp_load_weights.argtypes = [P, P, C.POINTER(C.c_char_p), C.c_int32, P, C.c_uint64, C.c_int32,
                                      C.POINTER(LoadStats)]
+    lib.atp_load_reshard_weights.argtypes = [P, P, C.POINTER(C.c_char_p), C.c_int32, P, C.c_uint64, P,
+                                             C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, P,
+                                             C.c_int32, C.POINTER(LoadStats)]
     lib.atp_kv_evict_lru.argtypes = [P, C.c_int32, C.c_int32, C.c_int64, P, C.c_uint64, C.c_uint64, C.c_int32,
                                      P, P, C.POINTER(EvictStats)]
     lib.atp_daemon_serve.argtypes = [C.c_char_p, C.c_int32]
@@ -297,6 +300,18 @@ class Plan:
         st = LoadStats()
         _check(lib.atp_load_weights(self.h, files.h, arr, len(names), inflow, inflow_bytes, threads,
                                     C.byref(st)))
+        return st
+
+    def load_reshard_weights(self, files: "StFiles", names, arena, arena_bytes, new_arena, new_bytes, inflow,
+                             inflow_bytes, outbound, outbound_bytes, staging, staging_bytes, compute, copy,
+                             threads=0) -> LoadStats:
+        """Range-read the weight inflow from `files` into the pinned buffer at
+        `inflow` while the weights reshard is enqueued behind the reads."""
+        arr = (C.c_char_p * len(names))(*[n.encode() for n in names])
+        st = LoadStats()
+        _check(lib.atp_load_reshard_weights(self.h, files.h, arr, len(names), arena, arena_bytes, new_arena,
+                                            new_bytes, inflow, inflow_bytes, outbound, outbound_bytes, staging,
+                                            staging_bytes, compute, copy, threads, C.byref(st)))
         return st
 
 

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <climits>
 #include <cstring>
+#include <functional>
 #include <string>
 
 #include "../../include/atp.h"
@@ -317,6 +318,35 @@ int atp_load_weights(const atp_plan_t *plan, const atp_st_t *st, const char *con
   return guard([&]() -> int {
     if (!plan || !st) return fail(ATP_EINVAL, "plan or st is NULL");
     atp::load_weights(*plan->p, *st->f, names, n_names, inflow_host, inflow_bytes, n_threads, stats);
+    return ATP_OK;
+  });
+}
+
+int atp_load_reshard_weights(atp_plan_t *plan, const atp_st_t *st, const char *const *names, int32_t n_names,
+                             void *arena, uint64_t arena_bytes, void *new_arena, uint64_t new_arena_bytes,
+                             void *inflow_host, uint64_t inflow_bytes, void *outbound_host, uint64_t outbound_bytes,
+                             void *staging, uint64_t staging_bytes, atp_stream compute, atp_stream copy,
+                             int32_t n_threads, atp_load_stats *stats) {
+  return guard([&]() -> int {
+    if (!plan || !st) return fail(ATP_EINVAL, "plan or st is NULL");
+    // checks the names and builds the reads before anything starts
+    atp::LoadJob job(*plan->p, *st->f, names, n_names, inflow_host, inflow_bytes, n_threads);
+    job.start();
+    const std::function<void(uint64_t)> await = [&job](uint64_t end) { job.await(end); };
+    atp::exec_call(*plan->p, false, arena, arena_bytes, new_arena, new_arena_bytes, inflow_host, inflow_bytes,
+                   outbound_host, outbound_bytes, nullptr, 0, staging, staging_bytes,
+                   static_cast<hipStream_t>(compute), static_cast<hipStream_t>(copy), &await);
+    try {
+      job.finish(stats);
+    } catch (...) {
+      // a read failed after the reshard was enqueued over the partly read
+      // buffer: let it drain before the caller may free anything
+      try {
+        atp::exec_sync(*plan->p, nullptr);
+      } catch (...) {
+      }
+      throw;
+    }
     return ATP_OK;
   });
 }

@@ -2,17 +2,21 @@
 #pragma once
 #include <hip/hip_runtime_api.h>
 
+#include <functional>
 #include <vector>
 
 #include "plan.h"
 
 namespace atp {
 
-// Enqueue one reshard call (weights: kvcall = false).  Throws Error.
+// Enqueue one reshard call (weights: kvcall = false).  Throws Error.  With
+// `await`, the host calls it with the end of each inflow piece's bytes in
+// the inflow buffer before issuing that piece, and it returns once those
+// bytes are there (the inflow buffer is still being filled).
 void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *new_arena, uint64_t new_bytes,
                const void *inflow_host, uint64_t inflow_bytes, void *outbound_host, uint64_t outbound_bytes,
                const int32_t *table, int64_t n_entries, void *staging, uint64_t staging_bytes, hipStream_t compute,
-               hipStream_t copy);
+               hipStream_t copy, const std::function<void(uint64_t)> *await = nullptr);
 int exec_sync(Plan &P, atp_timing *out);
 void exec_free(Plan &P);
 void exec_launches(const Plan &P, std::vector<atp_launch> &out);

@@ -196,6 +196,8 @@ constexpr float kSpinMarginMs = 0.15f;   // the empty kernel must finish this mu
 #endif
 constexpr uint64_t kHostReadGrid = ATP_HOST_READ_GRID;
 constexpr uint64_t kOutboundGrid = 8;
+// host-read launch pieces while the inflow buffer is still being filled
+constexpr uint64_t kPipeBytes = 64ull << 20;
 std::map<std::pair<hipStream_t, hipStream_t>, bool> g_same_queue;  // under g_pool_mu
 
 bool same_queue(Exec &E, hipStream_t a, hipStream_t b) {
@@ -412,7 +414,7 @@ void launch_copy(Exec &E, const Launch &L, const Desc *dev_desc, const int64_t *
 void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *new_arena, uint64_t new_bytes,
                const void *inflow_host, uint64_t inflow_bytes, void *outbound_host, uint64_t outbound_bytes,
                const int32_t *table, int64_t n_entries, void *staging, uint64_t staging_bytes, hipStream_t compute,
-               hipStream_t copy) {
+               hipStream_t copy, const std::function<void(uint64_t)> *await) {
   CallPlan &c = kvcall ? P.k : P.w;
   Exec &E = exec_of(P);
   CallState &cs = kvcall ? E.k : E.w;
@@ -510,6 +512,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   cs.h2d0 = E.ev_time();
   HIPCHK(hipEventRecord(cs.h2d0, copy));
   for (const HostCopy &h : c.directs) {
+    if (await) (*await)(h.host_off + h.bytes);
     HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
     cs.h2d_bytes += h.bytes;
   }
@@ -542,9 +545,11 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   }
 
   // the copy kernel reads inflow pieces from the pinned host buffer into
-  // their final place (kind 4 launches)
+  // their final place (kind 4 launches).  While the inflow buffer is still
+  // being filled (`await`), each launch is cut at descriptor boundaries into
+  // pieces of at least kPipeBytes, each issued once the bytes it reads are in.
   auto issue_host_reads = [&](hipStream_t s) {
-    for (const Launch &L : c.host_reads) {
+    auto one = [&](const Launch &L) {
       CallState::LaunchRec r{4, -1, L.bytes, E.ev_time(), E.ev_time()};
       HIPCHK(hipEventRecord(r.e0, s));
       launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s,
@@ -552,6 +557,28 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
       HIPCHK(hipEventRecord(r.e1, s));
       cs.launches.push_back(r);
       cs.h2d_bytes += L.bytes;
+    };
+    const int64_t nb = kvcall ? P.kv.num_blocks : 0, live = kvcall ? P.kv.live_blocks : 0;
+    for (const Launch &L : c.host_reads) {
+      if (!await) {
+        one(L);
+        continue;
+      }
+      Launch piece = L;
+      piece.bytes = 0;
+      uint64_t end = 0;
+      for (int d = L.d0; d < L.d1; ++d) {
+        const Fam &f = c.fams[size_t(d)];
+        piece.bytes += (f.o_end - f.o_begin) * f.rows * f.run;
+        end = std::max(end, extent(f, true, nb, live));  // source side: the inflow buffer
+        if (piece.bytes >= kPipeBytes || d + 1 == L.d1) {
+          piece.d1 = d + 1;
+          (*await)(end);
+          one(piece);
+          piece.d0 = d + 1;
+          piece.bytes = 0;
+        }
+      }
     }
     cs.hr1 = E.ev_time();
     HIPCHK(hipEventRecord(cs.hr1, s));

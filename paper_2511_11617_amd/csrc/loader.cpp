@@ -19,8 +19,10 @@
 #include <cctype>
 #include <cerrno>
 #include <chrono>
+#include <condition_variable>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <thread>
 
 namespace atp {
@@ -320,15 +322,65 @@ StFiles *st_open(const char *const *paths, int n) {
   return S.release();
 }
 
-void load_weights(const Plan &P, const StFiles &S, const char *const *names, int n_names, void *inflow,
-                  uint64_t inflow_bytes, int n_threads, atp_load_stats *st) {
+// ---- reads -------------------------------------------------------------------------
+
+struct LoadJob::Impl {
+  std::vector<ReadOp> ops;  // in buffer order: ops [0, k) cover [0, ops[k].dst - base)
+  char *base = nullptr;
+  uint64_t bytes = 0, tensor_bytes = 0;
+  int threads = 1;
+  size_t batch = 1, n_batches = 0;
+  std::atomic<size_t> next{0};
+  std::atomic<bool> bad{false};
+  std::mutex mu;
+  std::condition_variable cv;
+  std::vector<char> done;   // per batch, under mu
+  size_t front = 0;         // first batch not done, under mu
+  uint64_t ready = 0;       // buffer prefix read, under mu
+  bool failed = false;      // under mu
+  std::vector<std::thread> pool;
+  std::chrono::steady_clock::time_point t0;
+  double read_ms = 0;
+
+  void batch_done(size_t b, bool ok) {
+    std::lock_guard<std::mutex> g(mu);
+    if (!ok) {
+      failed = true;
+      ready = bytes;  // wake every waiter
+    } else {
+      done[b] = 1;
+      while (front < n_batches && done[front]) ++front;
+      if (!failed) ready = front < n_batches ? uint64_t(ops[front * batch].dst - base) : bytes;
+    }
+    cv.notify_all();
+  }
+  void work() {
+    while (!bad.load(std::memory_order_relaxed)) {
+      size_t i0 = next.fetch_add(batch);
+      if (i0 >= ops.size()) return;
+      size_t i1 = std::min(ops.size(), i0 + batch);
+      bool ok = true;
+      for (size_t i = i0; i < i1 && ok; ++i) ok = read_all(ops[i].fd, ops[i].off, ops[i].dst, ops[i].bytes);
+      if (!ok) bad = true;
+      batch_done(i0 / batch, ok);
+    }
+  }
+  void join() {
+    for (auto &th : pool) th.join();
+    pool.clear();
+  }
+};
+
+LoadJob::LoadJob(const Plan &P, const StFiles &S, const char *const *names, int n_names, void *inflow,
+                 uint64_t inflow_bytes, int n_threads)
+    : impl_(new Impl()) {
   const CallPlan &c = P.w;
+  Impl &J = *impl_;
   if (n_names != int(P.tp.size())) fail("one tensor name per problem tensor is needed");
   if (!names) fail("names is NULL");
   if (inflow_bytes != c.inflow || (c.inflow && !inflow)) fail("inflow buffer must hold exactly " + std::to_string(c.inflow) + " bytes");
   // tensors named by the plan, checked against the problem's shapes
   std::vector<const StTensor *> ft(P.tp.size(), nullptr);
-  uint64_t tensor_bytes = 0;
   for (size_t i = 0; i < P.tp.size(); ++i) {
     if (!names[i]) fail("tensor name " + std::to_string(i) + " is NULL");
     auto it = S.map.find(names[i]);
@@ -339,11 +391,13 @@ void load_weights(const Plan &P, const StFiles &S, const char *const *names, int
     if (f.shape.size() != 2 || f.shape[0] != uint64_t(t.rows) || f.shape[1] != uint64_t(t.cols))
       fail(std::string("tensor '") + names[i] + "' has another shape than the problem's [rows, cols]");
     ft[i] = &f;
-    tensor_bytes += f.end - f.begin;
+    J.tensor_bytes += f.end - f.begin;
   }
   // the byte intervals of every inflow segment, in buffer order
-  std::vector<ReadOp> ops;
+  std::vector<ReadOp> &ops = J.ops;
   char *base = static_cast<char *>(inflow);
+  J.base = base;
+  J.bytes = c.inflow;
   for (const atp_segment &s : c.seg_in) {
     const atp_tensor &t = P.tp[size_t(s.tensor)].t;
     const StTensor &f = *ft[size_t(s.tensor)];
@@ -379,38 +433,54 @@ void load_weights(const Plan &P, const StFiles &S, const char *const *names, int
     }
     if (got != s.bytes) throw Error(ATP_EINVAL, "inflow segment size disagrees with its tensor");
   }
-  // read them on a pool of threads, in balanced byte batches
+  // balanced byte batches, taken in buffer order by a pool of threads
   unsigned hw = std::max(1u, std::thread::hardware_concurrency());
-  int threads = n_threads > 0 ? n_threads : int(std::min(16u, hw));
-  threads = std::max(1, std::min<int>(threads, int(std::max<size_t>(ops.size(), 1))));
-  auto t0 = std::chrono::steady_clock::now();
-  std::atomic<size_t> next{0};
-  std::atomic<bool> bad{false};
-  const size_t batch = std::max<size_t>(1, ops.size() / (size_t(threads) * 64));
-  auto work = [&]() {
-    while (!bad.load(std::memory_order_relaxed)) {
-      size_t i0 = next.fetch_add(batch);
-      if (i0 >= ops.size()) return;
-      size_t i1 = std::min(ops.size(), i0 + batch);
-      for (size_t i = i0; i < i1; ++i)
-        if (!read_all(ops[i].fd, ops[i].off, ops[i].dst, ops[i].bytes)) {
-          bad = true;
-          return;
-        }
-    }
-  };
-  std::vector<std::thread> pool;
-  for (int i = 1; i < threads; ++i) pool.emplace_back(work);
-  work();
-  for (auto &th : pool) th.join();
-  if (bad) fail("a range read failed (file shorter than its header says, or an I/O error)");
-  if (st) {
-    st->read_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
-    st->bytes = c.inflow;
-    st->reads = ops.size();
-    st->tensor_bytes = tensor_bytes;
-    st->threads = threads;
+  J.threads = n_threads > 0 ? n_threads : int(std::min(16u, hw));
+  J.threads = std::max(1, std::min<int>(J.threads, int(std::max<size_t>(ops.size(), 1))));
+  J.batch = std::max<size_t>(1, ops.size() / (size_t(J.threads) * 64));
+  J.n_batches = (ops.size() + J.batch - 1) / J.batch;
+  J.done.assign(J.n_batches, 0);
+  J.ready = ops.empty() ? J.bytes : 0;
+}
+
+LoadJob::~LoadJob() {
+  if (impl_) {
+    impl_->bad = true;  // stop taking batches
+    impl_->join();
   }
+}
+
+void LoadJob::start() {
+  Impl &J = *impl_;
+  J.t0 = std::chrono::steady_clock::now();
+  for (int i = 0; i < J.threads; ++i) J.pool.emplace_back([&J]() { J.work(); });
+}
+
+void LoadJob::await(uint64_t end) {
+  Impl &J = *impl_;
+  std::unique_lock<std::mutex> g(J.mu);
+  J.cv.wait(g, [&]() { return J.ready >= std::min(end, J.bytes) || J.failed; });
+}
+
+void LoadJob::finish(atp_load_stats *st) {
+  Impl &J = *impl_;
+  J.join();
+  J.read_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - J.t0).count();
+  if (J.failed) fail("a range read failed (file shorter than its header says, or an I/O error)");
+  if (st) {
+    st->read_ms = J.read_ms;
+    st->bytes = J.bytes;
+    st->reads = J.ops.size();
+    st->tensor_bytes = J.tensor_bytes;
+    st->threads = J.threads;
+  }
+}
+
+void load_weights(const Plan &P, const StFiles &S, const char *const *names, int n_names, void *inflow,
+                  uint64_t inflow_bytes, int n_threads, atp_load_stats *st) {
+  LoadJob job(P, S, names, n_names, inflow, inflow_bytes, n_threads);
+  job.start();
+  job.finish(st);
 }
 
 }  // namespace atp

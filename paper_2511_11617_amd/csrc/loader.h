@@ -34,4 +34,26 @@ StFiles *st_open(const char *const *paths, int n);
 void load_weights(const Plan &P, const StFiles &S, const char *const *names, int n_names, void *inflow,
                   uint64_t inflow_bytes, int n_threads, atp_load_stats *stats);
 
+// The same reads run on background threads, with the byte prefix of the
+// buffer they have completed observable: a reshard can issue each inflow
+// piece as soon as the bytes under it have landed.  The constructor checks
+// the names and builds the reads (throws Error, nothing started); start()
+// launches the threads; await(end) blocks until [0, end) is read or a read
+// failed; finish() joins them and throws Error if a read failed.  The
+// destructor stops and joins threads still running.
+class LoadJob {
+ public:
+  LoadJob(const Plan &P, const StFiles &S, const char *const *names, int n_names, void *inflow,
+          uint64_t inflow_bytes, int n_threads);
+  ~LoadJob();
+  void start();
+  void await(uint64_t end);
+  void finish(atp_load_stats *stats);
+
+  struct Impl;
+
+ private:
+  std::unique_ptr<Impl> impl_;
+};
+
 }  // namespace atp

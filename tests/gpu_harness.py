@@ -59,11 +59,16 @@ def say(msg):
 
 
 def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
-             ckpt_dir=None, evict=None):
+             ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False):
     """Reshard one workload on the GPU and compare with the oracle.  With
     `ckpt_dir`, the weight inflow is read from a safetensors checkpoint
     written there by the library's range-read loader instead of being copied
-    from the oracle's packed inflow.  With `evict` = (last_use, budget
+    from the oracle's packed inflow; with `pipelined` too, the reads and the
+    weights reshard run together (atp_load_reshard_weights).  A
+    `sparse_ckpt` holds only the intervals the plan reads (the oracle's
+    packed inflow put back at its tensor coordinates), holes elsewhere.
+    `kv_first` issues the KV call before the weights call (out of place
+    only: in place that order is refused).  With `evict` = (last_use, budget
     fraction of the new KV demand), the oracle's LRU policy picks the kept
     sessions; the old arena holds every session, the reshard gets the kept
     rows, and with ATP_KV_COMPACT the result is the oracle's compact arena."""
@@ -128,13 +133,28 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
         from synth import checkpoint
         tl = problem.tensor_list(c)
         path = os.path.join(str(ckpt_dir), "model.safetensors")
-        checkpoint.write_package(path, Content(c["seed"], c["w_kind"], c["kv_kind"]),
-                                 [(n, l, r, cc) for (n, l, k, sp, r, cc, u) in tl],
-                                 "fp16" if c["w_kind"] == KIND_FP16 else "bf16")
+        tens = [(n, l, r, cc) for (n, l, k, sp, r, cc, u) in tl]
+        dtype = "fp16" if c["w_kind"] == KIND_FP16 else "bf16"
+        if sparse_ckpt:
+            regions = []
+            for sg in plan.segments(atp.SEG_INFLOW_W):
+                n, l, kind, sp, rows, cols, unit = tl[sg.tensor]
+                a, b = sg.unit_begin * unit, sg.unit_end * unit
+                w = in_w[sg.host_offset:sg.host_offset + sg.bytes].view(np.uint16)
+                if kind == atp.ROWS:
+                    regions.append((n, l, cols, a, b, 0, cols, w.reshape(b - a, cols)))
+                else:
+                    regions.append((n, l, cols, 0, rows, a, b, w.reshape(rows, b - a)))
+            checkpoint.write_stream(path, tens, regions, dtype)
+        else:
+            checkpoint.write_package(path, Content(c["seed"], c["w_kind"], c["kv_kind"]), tens, dtype)
         hin_w.fill_(0xA5)  # the loader must write every byte
         files = atp.StFiles([path])
-        plan.load_weights(files, [checkpoint.name(n, l) for (n, l, *_) in tl], hin_w.data_ptr(), in_w.size)
-        files.close()
+        ckpt_names = [checkpoint.name(n, l) for (n, l, *_) in tl]
+        if not pipelined:
+            plan.load_weights(files, ckpt_names, hin_w.data_ptr(), in_w.size)
+            files.close()
+            files = None
     hout_w = torch.full((max(st.outbound_w, 1),), 0x3C, dtype=u8, pin_memory=True)
     hout_k = torch.full((max(st.outbound_kv, 1),), 0x3C, dtype=u8, pin_memory=True)
     table_d = torch.from_numpy(table).to(dev)
@@ -143,13 +163,30 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
     torch.cuda.synchronize()
 
     ptr = lambda t: t.data_ptr() if t is not None else None
-    plan.reshard_weights(ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0,
-                         ptr(hin_w), in_w.size, ptr(hout_w), st.outbound_w, ptr(stage_w), stage_w.numel(),
-                         compute.cuda_stream, copy.cuda_stream)
-    plan.reshard_kv(ptr(ak), ak.numel(), ptr(nk), nk.numel() if nk is not None else 0,
-                    ptr(table_d), table.shape[0], table.shape[1], ptr(hin_k), in_k.size,
-                    ptr(hout_k), st.outbound_kv, ptr(stage_k), stage_k.numel(),
-                    compute.cuda_stream, copy.cuda_stream)
+    w_args = (ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0, ptr(hin_w), in_w.size,
+              ptr(hout_w), st.outbound_w, ptr(stage_w), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
+
+    def weights_call():
+        if ckpt_dir is not None and in_w.size and pipelined:
+            ls = plan.load_reshard_weights(files, ckpt_names, *w_args)
+            assert ls.bytes == in_w.size
+            files.close()
+        else:
+            plan.reshard_weights(*w_args)
+
+    def kv_call():
+        plan.reshard_kv(ptr(ak), ak.numel(), ptr(nk), nk.numel() if nk is not None else 0,
+                        ptr(table_d), table.shape[0], table.shape[1], ptr(hin_k), in_k.size,
+                        ptr(hout_k), st.outbound_kv, ptr(stage_k), stage_k.numel(),
+                        compute.cuda_stream, copy.cuda_stream)
+
+    if kv_first:
+        assert not inplace, "in place the weights call comes first"
+        kv_call()
+        weights_call()
+    else:
+        weights_call()
+        kv_call()
     t = plan.sync()
     torch.cuda.synchronize()
 

@@ -37,3 +37,39 @@ def test_tiny_from_checkpoint(tmp_path, seed, experts):
 def test_full_reload_from_checkpoint(tmp_path):
     run_case(configs.get(1, w_kind=KIND_TAG16), flags=atp.PLAN_FULL, variant="full", ckpt_dir=tmp_path,
              name="cfg1-full-ckpt")
+
+
+# ---- the reads pipelined with the weights reshard (atp_load_reshard_weights) ----
+
+@pytest.mark.parametrize("flags", [0, atp.INPLACE])
+def test_cfg1_pipelined_from_checkpoint(tmp_path, flags):
+    run_case(configs.get(1, w_kind=KIND_TAG16), flags=flags, ckpt_dir=tmp_path, pipelined=True,
+             name="cfg1-ckpt-pipelined")
+
+
+@pytest.mark.parametrize("seed,experts", [(3, True), (8, False)])
+def test_tiny_pipelined_from_checkpoint(tmp_path, seed, experts):
+    run_case(tiny_cfg(random.Random(seed), experts), ckpt_dir=tmp_path, pipelined=True,
+             name=f"tiny{seed}-ckpt-pipelined")
+
+
+@pytest.mark.parametrize("seed,experts", [(4, False), (9, True)])
+def test_tiny_pipelined_after_the_kv_call(tmp_path, seed, experts):
+    """Out of place the KV call may come first: its inflow then uses the link
+    while the weight reads run."""
+    run_case(tiny_cfg(random.Random(seed), experts), ckpt_dir=tmp_path, pipelined=True, kv_first=True,
+             name=f"tiny{seed}-ckpt-pipelined-kv-first")
+
+
+def test_large_layer_pipelined_from_checkpoint(tmp_path):
+    """One layer of the 40-layer TP 4->3 shape: 110 MB of weight inflow, so
+    the host reads go out in several pieces as the reads complete (the
+    checkpoint holds the intervals read, holes elsewhere)."""
+    c = configs.scaled(2, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    run_case(c, ckpt_dir=tmp_path, pipelined=True, sparse_ckpt=True, name="dense40-1layer-ckpt-pipelined")
+
+
+def test_large_layer_pipelined_after_the_kv_call(tmp_path):
+    c = configs.scaled(2, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    run_case(c, ckpt_dir=tmp_path, pipelined=True, sparse_ckpt=True, kv_first=True,
+             name="dense40-1layer-ckpt-pipelined-kv-first")

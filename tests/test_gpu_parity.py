@@ -54,6 +54,13 @@ def test_random_small(seed):
     run_case(c, name=f"random-{seed}")
 
 
+@pytest.mark.parametrize("seed", list(range(6)))
+def test_random_small_kv_call_first(seed):
+    """Out of place the two calls may come in either order."""
+    rng = random.Random(500 + seed)
+    run_case(tiny_cfg(rng, experts=seed % 2 == 1), kv_first=True, name=f"random-kv-first-{seed}")
+
+
 @pytest.mark.parametrize("seed", list(range(24)))
 def test_random_small_in_place(seed):
     rng = random.Random(1000 + seed)

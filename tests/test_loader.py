@@ -161,6 +161,12 @@ def test_missing_and_mismatched_tensors(tmp_path):
     swapped[0], swapped[1] = swapped[1], swapped[0]   # wq <-> wk: other shape
     _expect_einval(lambda: plan.load_weights(files, swapped, buf.ctypes.data, n_in), "shape")
     _expect_einval(lambda: plan.load_weights(files, names, buf.ctypes.data, n_in - 2), "exactly")
+    # the pipelined reload checks the same before any read or GPU work starts
+    no_gpu = (None, 0, None, 0)
+    _expect_einval(lambda: plan.load_reshard_weights(files, names[:-1], 0, 0, 0, 0, buf.ctypes.data, n_in,
+                                                     *no_gpu, None, None), "one tensor name")
+    _expect_einval(lambda: plan.load_reshard_weights(files, swapped, 0, 0, 0, 0, buf.ctypes.data, n_in,
+                                                     *no_gpu, None, None), "shape")
     files.close()
     # same shapes, 4-byte elements
     tens, _ = _tensors(c)
