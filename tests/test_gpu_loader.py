@@ -73,3 +73,46 @@ def test_large_layer_pipelined_after_the_kv_call(tmp_path):
     c = configs.scaled(2, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
     run_case(c, ckpt_dir=tmp_path, pipelined=True, sparse_ckpt=True, kv_first=True,
              name="dense40-1layer-ckpt-pipelined-kv-first")
+
+
+def test_pipelined_read_failure_drains_and_reports(tmp_path):
+    """A read that fails after part of the reshard is enqueued (the file is
+    cut short after it was opened): the call drains the enqueued work, then
+    reports ATP_EINVAL; nothing is left pending and the next reshard works.
+    The condition is made on the host: every kernel runs in bounds."""
+    import os
+
+    import numpy as np
+
+    from oracle import model, repack
+    from paper_2511_11617_amd import problem
+    from synth import checkpoint, pagetable
+    from synth.content import Content
+
+    c = configs.get(1, w_kind=KIND_TAG16)
+    table, pool = pagetable.make_for(c)
+    plan = problem.build(c, n_live=len(repack.live_blocks(table)), pool=pool).plan()
+    st = plan.stats()
+    tl = problem.tensor_list(c)
+    path = str(tmp_path / "model.safetensors")
+    checkpoint.write_package(path, Content(c["seed"], c["w_kind"], c["kv_kind"]),
+                             [(n, l, r, cc) for (n, l, k, sp, r, cc, u) in tl], "bf16")
+    files = atp.StFiles([path])
+    os.truncate(path, os.path.getsize(path) // 2)  # reads past the middle come back short
+    dev = torch.device("cuda")
+    u8 = torch.uint8
+    aw = torch.zeros(max(st.old_arena_bytes, 256), dtype=u8, device=dev)
+    nw = torch.zeros(max(st.new_arena_bytes, 256), dtype=u8, device=dev)
+    sw = torch.zeros(max(st.staging_w, 256), dtype=u8, device=dev)
+    hw = torch.zeros(max(st.inflow_w, 1), dtype=u8, pin_memory=True)
+    s0, s1 = torch.cuda.current_stream(), torch.cuda.Stream()
+    with pytest.raises(atp.AtpError) as e:
+        plan.load_reshard_weights(files, [checkpoint.name(n, l) for (n, l, *_) in tl], aw.data_ptr(), aw.numel(),
+                                  nw.data_ptr(), nw.numel(), hw.data_ptr(), st.inflow_w, None, 0, sw.data_ptr(),
+                                  sw.numel(), s0.cuda_stream, s1.cuda_stream)
+    assert e.value.code == atp.EINVAL and "range read failed" in str(e.value)
+    files.close()
+    plan.sync()  # nothing pending: returns at once
+    torch.cuda.synchronize()
+    del aw, nw, sw, hw
+    run_case(configs.get(1, w_kind=KIND_TAG16), name="cfg1-after-a-failed-read")
