@@ -16,7 +16,7 @@ from paper_2511_11617_amd import atp
 from synth import configs
 from synth.content import KIND_RAW16, KIND_TAG16
 from tests.gpu_harness import SQUEEZED_RING_CAP, run_case, squeezed_ring_cfg
-from tests.test_oracle_repack import tiny_cfg
+from tests.test_oracle_repack import med_cfg, tiny_cfg
 from tests.test_schedule_sim import single_target_cfg
 
 pytestmark = pytest.mark.gpu
@@ -59,6 +59,16 @@ def test_random_small_kv_call_first(seed):
     """Out of place the two calls may come in either order."""
     rng = random.Random(500 + seed)
     run_case(tiny_cfg(rng, experts=seed % 2 == 1), kv_first=True, name=f"random-kv-first-{seed}")
+
+
+@pytest.mark.parametrize("mode", ["out-of-place", "in-place", "kv-first"])
+@pytest.mark.parametrize("seed", list(range(20)))
+def test_random_medium(seed, mode):
+    """Random medium decoders: real 2-4 KiB KV head lines (wide tiles),
+    multi-tile weight lines, up to TP 8, fragmented pools."""
+    c = med_cfg(random.Random(9000 + seed), experts=seed % 3 == 0)
+    run_case(c, flags=atp.INPLACE if mode == "in-place" else 0, kv_first=mode == "kv-first",
+             name=f"random-medium-{seed}-{mode}")
 
 
 @pytest.mark.parametrize("seed", list(range(24)))

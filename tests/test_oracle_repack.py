@@ -54,6 +54,39 @@ def tiny_cfg(rng: random.Random, experts=False):
     return c
 
 
+def med_cfg(rng: random.Random, experts=False):
+    """A random medium decoder and TP change: head_dim 64/128 with 16-token
+    blocks (2-4 KiB KV head lines), hidden 256-1024, up to TP 8, fragmented
+    pools, unequal old q splits, dense or MoE."""
+    N = rng.randint(2, 8)
+    nf = rng.randint(1, min(3, N - 1))
+    failed = sorted(rng.sample(range(N), nf))
+    M = N - nf
+    hd = rng.choice([64, 128])
+    n_kv = rng.choice([1, 2, 4, 8])
+    g = rng.choice([1, 2, 4])
+    n_q = max(n_kv * g, n_kv * (-(-N // n_kv)))
+    kw = dict(layers=rng.randint(1, 3), hidden=rng.choice([256, 512, 1024]), n_q=n_q, n_kv=n_kv,
+              head_dim=hd, old_tp=N, new_tp=M, failed=failed,
+              self_old=rng.choice([i for i in range(N) if i not in failed]),
+              n_seq=rng.randint(1, 12), seq_tokens=rng.choice([64, 128, 256, 512]), block_tokens=16,
+              fragmented=rng.random() < 0.5, pool_factor=1.25, seed=rng.randint(0, 999),
+              w_kind=KIND_TAG16, kv_kind=rng.choice([KIND_TAG16, KIND_RAW16]),
+              new_q_widths=None, new_kv_widths=None, new_ffn_widths=None, new_expert_widths=None,
+              kv_layout=rng.choice(["head", "head", "token"]))
+    if experts:
+        kw.update(experts=rng.randint(N, 3 * N), expert_ffn=rng.choice([64, 128, 256]), ffn=0)
+    else:
+        unit = rng.choice([1, 8, 16])
+        kw.update(ffn=unit * rng.randint(N, 16 * N), ffn_unit=unit, experts=0)
+    c = configs.get(1, **kw)
+    if rng.random() < 0.5:
+        cuts = sorted(rng.sample(range(1, n_q), N - 1))
+        b = [0] + cuts + [n_q]
+        c["old_ranges"] = {"q": [(b[i], b[i + 1]) for i in range(N)]}
+    return c
+
+
 def _check_cfg(c):
     pb = model.build(c)
     content = Content(c["seed"], c["w_kind"], c["kv_kind"])

@@ -19,7 +19,7 @@ from synth.content import KIND_TAG16, Content
 from tests.gpu_harness import SQUEEZED_RING_CAP, CachedContent, squeezed_ring_cfg
 from tests.schedule_sim import (D2H, H2D, INFLOW, NEW, OLD, OUTBOUND, REPACK, STAGING, Copy, Hazard,
                                  copies, replay)
-from tests.test_oracle_repack import tiny_cfg
+from tests.test_oracle_repack import med_cfg, tiny_cfg
 
 
 def sim_case(c, flags=0, staging_cap=0, assign="inorder", mutate=None):
@@ -82,6 +82,12 @@ def test_cfg1_survivors_in_place(self_old):
 def test_random_small(seed, experts, inplace):
     c = tiny_cfg(random.Random(seed), experts)
     sim_case(c, flags=atp.INPLACE if inplace else 0)
+
+
+@pytest.mark.parametrize("seed", list(range(10)))
+def test_random_medium(seed):
+    c = med_cfg(random.Random(9000 + seed), experts=seed % 3 == 0)
+    sim_case(c, flags=atp.INPLACE if seed % 2 else 0)
 
 
 @settings(max_examples=40, deadline=None)
