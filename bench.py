@@ -152,6 +152,12 @@ def main():
                               "global_reload_bytes": int(a.global_reload)}
         except atp.AtpError as e:
             assignment[nm] = {"error": str(e)}
+    if args.plan != "full":  # a full reload lands the whole shard whatever it holds
+        by_target = inflow_by_target(cfg, built, plan, cfg["self_old"])
+        if by_target[st.self_new_rank] == st.inflow_w + st.inflow_kv:  # the plan's own inflow
+            assignment["self_inflow_by_target_bytes"] = by_target
+            assignment["self_inflow_min_bytes"] = min(by_target)
+            assignment["critical_path"] = critical_path(cfg, n_live, pool, flags, cap)
     dev = torch.device("cuda")
     u8 = torch.uint8
     content = Content(cfg["seed"], cfg["w_kind"], cfg["kv_kind"])
@@ -379,6 +385,45 @@ def main():
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, aw, ak, hin_w.tensor, hin_k.tensor,
                                            table, pool)
     print(json.dumps(out), flush=True)
+
+
+def inflow_by_target(cfg, built, plan, self_old):
+    """Bytes this survivor would land if it hosted each new target: the
+    target's units it does not hold, in every tensor and in the KV cache
+    (library ranges and shapes only)."""
+    from paper_2511_11617_amd import atp
+    eb = cfg["elem_bytes"]
+    out = []
+    for j in range(cfg["new_tp"]):
+        def miss(sp):
+            nb, ne = plan.ranges(sp)[j]
+            ob, oe = built.old_ranges[sp][self_old]
+            return (ne - nb) - max(0, min(ne, oe) - max(nb, ob))
+        tot = sum(miss(sp) * unit * (cols if kind == atp.ROWS else rows) * eb
+                  for (name, l, kind, sp, rows, cols, unit) in built.tensors)
+        tot += miss(1) * built.n_live * cfg["block_tokens"] * cfg["head_dim"] * eb * 2 * cfg["layers"]
+        out.append(int(tot))
+    return out
+
+
+def critical_path(cfg, n_live, pool, flags, cap):
+    """Every survivor's inflow by target: the largest under the in-order
+    assignment (the recovery ends with that survivor) against the smallest
+    largest over all M! assignments (host planning only)."""
+    import itertools
+
+    from paper_2511_11617_amd import problem
+    surv = [r for r in range(cfg["old_tp"]) if r not in cfg["failed"]]
+    A = []
+    for so in surv:
+        c = dict(cfg, self_old=so)
+        b = problem.build(c, n_live=n_live, pool=pool, flags=flags, staging_cap=cap)
+        A.append(inflow_by_target(c, b, b.plan(), so))
+    M = len(A[0])
+    inorder = max(A[i][i] for i in range(M))
+    best = min(max(A[i][p[i]] for i in range(M)) for p in itertools.permutations(range(M))) if M <= 8 else None
+    return {"inorder_max_inflow_bytes": inorder, "best_max_inflow_bytes": best,
+            "critical_old_rank": surv[max(range(M), key=lambda i: A[i][i])]}
 
 
 def dominant_launch(launches):
