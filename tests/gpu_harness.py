@@ -59,7 +59,7 @@ def say(msg):
 
 
 def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
-             ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False):
+             ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False):
     """Reshard one workload on the GPU and compare with the oracle.  With
     `ckpt_dir`, the weight inflow is read from a safetensors checkpoint
     written there by the library's range-read loader instead of being copied
@@ -68,7 +68,8 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
     `sparse_ckpt` holds only the intervals the plan reads (the oracle's
     packed inflow put back at its tensor coordinates), holes elsewhere.
     `kv_first` issues the KV call before the weights call (out of place
-    only: in place that order is refused).  With `evict` = (last_use, budget
+    only: in place that order is refused).  `one_stream` passes the same
+    stream as compute and copy stream.  With `evict` = (last_use, budget
     fraction of the new KV demand), the oracle's LRU policy picks the kept
     sessions; the old arena holds every session, the reshard gets the kept
     rows, and with ATP_KV_COMPACT the result is the oracle's compact arena."""
@@ -159,7 +160,7 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
     hout_k = torch.full((max(st.outbound_kv, 1),), 0x3C, dtype=u8, pin_memory=True)
     table_d = torch.from_numpy(table).to(dev)
     compute = torch.cuda.current_stream()
-    copy = torch.cuda.Stream()
+    copy = compute if one_stream else torch.cuda.Stream()
     torch.cuda.synchronize()
 
     ptr = lambda t: t.data_ptr() if t is not None else None

@@ -199,3 +199,13 @@ def test_warmup_then_reshard():
     torch.cuda.synchronize()
     for flags in (0, atp.INPLACE):
         run_case(configs.get(1), flags=flags, name=f"after-warmup-flags{flags}")
+
+
+@pytest.mark.parametrize("flags", [0, atp.INPLACE])
+def test_one_stream_for_compute_and_copy(flags):
+    """The caller may pass one stream as both: the landings then queue behind
+    the repack on it, the side stream still comes from another hardware
+    queue, and the result is the same."""
+    run_case(configs.get(1), flags=flags, one_stream=True, name=f"one-stream-flags{flags}")
+    c = configs.scaled(2, layers=1, n_seq=2, seq_tokens=256)
+    run_case(c, flags=flags, one_stream=True, name=f"one-stream-dense40-flags{flags}")
