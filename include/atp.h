@@ -24,7 +24,10 @@
  *     return; atp_sync blocks.
  *   - Bytes are copied, never converted: any 16-bit payload (NaN, -0,
  *     denormals) arrives unchanged.
- *   - Threading: a plan is used by one host thread at a time.
+ *   - Threading: a plan is used by one host thread at a time.  Several
+ *     plans may be pending on one device at once, each on buffers of its
+ *     own; those issued on the same (compute, copy) pair run their side
+ *     work in issue order.
  */
 #ifndef ATP_H
 #define ATP_H

@@ -60,6 +60,13 @@ def say(msg):
 
 def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
              ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False):
+    return prepare_case(c, flags, staging_cap, assign, check_outbound, name, variant, ckpt_dir, evict, pipelined,
+                        sparse_ckpt, kv_first, one_stream)()()
+
+
+def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
+               ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False,
+               streams=None):
     """Reshard one workload on the GPU and compare with the oracle.  With
     `ckpt_dir`, the weight inflow is read from a safetensors checkpoint
     written there by the library's range-read loader instead of being copied
@@ -69,7 +76,12 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
     packed inflow put back at its tensor coordinates), holes elsewhere.
     `kv_first` issues the KV call before the weights call (out of place
     only: in place that order is refused).  `one_stream` passes the same
-    stream as compute and copy stream.  With `evict` = (last_use, budget
+    stream as compute and copy stream.
+
+    prepare_case() builds the plan and the device and host buffers and
+    returns issue(), which enqueues the reshard and returns finish(), which
+    syncs and checks it: several plans can then be pending together, on the
+    `streams` (compute, copy) given.  run_case() does all three.  With `evict` = (last_use, budget
     fraction of the new KV demand), the oracle's LRU policy picks the kept
     sessions; the old arena holds every session, the reshard gets the kept
     rows, and with ATP_KV_COMPACT the result is the oracle's compact arena."""
@@ -159,8 +171,11 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
     hout_w = torch.full((max(st.outbound_w, 1),), 0x3C, dtype=u8, pin_memory=True)
     hout_k = torch.full((max(st.outbound_kv, 1),), 0x3C, dtype=u8, pin_memory=True)
     table_d = torch.from_numpy(table).to(dev)
-    compute = torch.cuda.current_stream()
-    copy = compute if one_stream else torch.cuda.Stream()
+    if streams is not None:
+        compute, copy = streams
+    else:
+        compute = torch.cuda.current_stream()
+        copy = compute if one_stream else torch.cuda.Stream()
     torch.cuda.synchronize()
 
     ptr = lambda t: t.data_ptr() if t is not None else None
@@ -181,25 +196,34 @@ def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, n
                         ptr(hout_k), st.outbound_kv, ptr(stage_k), stage_k.numel(),
                         compute.cuda_stream, copy.cuda_stream)
 
-    if kv_first:
-        assert not inplace, "in place the weights call comes first"
-        kv_call()
-        weights_call()
-    else:
-        weights_call()
-        kv_call()
-    t = plan.sync()
-    torch.cuda.synchronize()
+    def issue():
+        if kv_first:
+            assert not inplace, "in place the weights call comes first"
+            kv_call()
+            weights_call()
+        else:
+            weights_call()
+            kv_call()
+        return finish
 
-    got_w = (aw if inplace else nw).cpu().numpy()[:want_w.size]
-    got_k = (ak if inplace else nk).cpu().numpy()[:want_k.size]
-    bad_w = np.flatnonzero(got_w[mask_w] != want_w[mask_w])
-    bad_k = np.flatnonzero(got_k[mask_k] != want_k[mask_k])
-    assert bad_w.size == 0, f"weights: {bad_w.size} wrong bytes, first at live byte {bad_w[:5]}"
-    assert bad_k.size == 0, f"kv: {bad_k.size} wrong bytes, first at live byte {bad_k[:5]}"
-    if inplace and check_outbound:
-        ow = repack.packed_weight_outbound(pb, content)
-        ok = repack.packed_kv_outbound(pb, content, table, pool)
-        np.testing.assert_array_equal(hout_w.numpy()[:ow.size], ow)
-        np.testing.assert_array_equal(hout_k.numpy()[:ok.size], ok)
-    return t, plan, st
+    def finish():
+        t = plan.sync()
+        torch.cuda.synchronize()
+        got_w = (aw if inplace else nw).cpu().numpy()[:want_w.size]
+        got_k = (ak if inplace else nk).cpu().numpy()[:want_k.size]
+        bad_w = np.flatnonzero(got_w[mask_w] != want_w[mask_w])
+        bad_k = np.flatnonzero(got_k[mask_k] != want_k[mask_k])
+        assert bad_w.size == 0, f"weights: {bad_w.size} wrong bytes, first at live byte {bad_w[:5]}"
+        assert bad_k.size == 0, f"kv: {bad_k.size} wrong bytes, first at live byte {bad_k[:5]}"
+        if inplace and check_outbound:
+            ow = repack.packed_weight_outbound(pb, content)
+            ok = repack.packed_kv_outbound(pb, content, table, pool)
+            np.testing.assert_array_equal(hout_w.numpy()[:ow.size], ow)
+            np.testing.assert_array_equal(hout_k.numpy()[:ok.size], ok)
+        return t, plan, st
+
+    # the calls hold raw pointers: every buffer stays referenced until the
+    # plan is synced, or the caching allocators would hand its memory to the
+    # next case's tensors while this plan still reads and writes it
+    finish.keep = (aw, nw, ak, nk, stage_w, stage_k, hin_w, hin_k, hout_w, hout_k, table_d)
+    return issue
