@@ -80,9 +80,12 @@ def parse():
     ap.add_argument("--state", action="store_true",
                     help="run the workload in place on memory the state plane holds: a writer process "
                          "allocates one weight and one KV region per layer group through the daemon and "
-                         "exits; this process maps them (timed) and reshards group after group")
+                         "exits; this process maps them (timed) and reshards every group")
     ap.add_argument("--state-groups", type=int, default=0,
                     help="layer groups of the state leg (default: the fewest whose regions fit)")
+    ap.add_argument("--state-window", type=int, default=0,
+                    help="groups of the state leg pending at once, each with staging and host buffers of "
+                         "its own (default 1: one group after another, the faster order in place)")
     ap.add_argument("--state-writer", default=None, help=argparse.SUPPRESS)
     ap.add_argument("--state-regions", default="", help=argparse.SUPPRESS)
     return ap.parse_args()
@@ -467,9 +470,14 @@ def state_main(args):
     """The workload in place on device memory the state plane owns
     (Sec. III-A).  IPC regions stay under 2 GiB, so the layers are split into
     the fewest balanced groups whose weight and KV regions fit; every layer
-    group is a reshard of its own (layers are independent in the plan), run
-    one after the other with a fresh plan each.  Timed: the attach (connect,
-    open every region, fetch the block table) once, and every step."""
+    group is a reshard of its own (layers are independent in the plan) with
+    a fresh plan each, one after another.  `--state-window W` keeps up to W
+    groups pending at once, each on staging and host buffers of its own; in
+    place that is slower: every group's weights chain (outbound reads,
+    levels, inflow read by the copy kernel) runs in turn on the one side
+    stream, while the later groups' KV inflow takes the link from it.
+    Timed: the attach (connect, open every region, fetch the block table)
+    once, and every step."""
     import subprocess
     import tempfile
 
@@ -510,24 +518,28 @@ def state_main(args):
         if not n_groups:
             raise SystemExit("one layer's arena exceeds the state plane's region limit")
     groups = split(n_groups)
+    window = min(args.state_window or 1, n_groups)
+    if window < 1:
+        raise SystemExit("--state-window must be at least 1")
     regions = []
     for i, g in enumerate(groups):
         wb, kb = sizes(g)
         regions += [(f"w{i}", wb), (f"k{i}", kb)]
     log(f"[state] workload {args.workload} {cfg['name']} in place: {n_groups} layer groups {groups}, "
-        f"{len(regions)} regions, {sum(n for _, n in regions) / 1e9:.2f} GB")
+        f"{len(regions)} regions, {sum(n for _, n in regions) / 1e9:.2f} GB, {window} pending at once")
 
     dev = torch.device("cuda")
     u8 = torch.uint8
     sts = [stats[g] for g in set(groups)]
-    stage_w = torch.empty(max(max(s.staging_w for s in sts), 256), dtype=u8, device=dev)
-    stage_k = torch.empty(max(max(s.staging_kv for s in sts), 256), dtype=u8, device=dev)
-    # one host buffer of each kind serves every group in turn: the groups run
-    # one after the other, and what the bytes are does not change the cost
-    hin_w = Pinned(max(s.inflow_w for s in sts))
-    hin_k = Pinned(max(s.inflow_kv for s in sts))
-    hout_w = Pinned(max(s.outbound_w for s in sts))
-    hout_k = Pinned(max(s.outbound_kv for s in sts))
+    # one set of staging and host buffers per pending group, reused by the
+    # groups that follow it (what the inflow bytes are does not change the cost)
+    slots = []
+    for _ in range(window):
+        slots.append(dict(
+            stage_w=torch.empty(max(max(s.staging_w for s in sts), 256), dtype=u8, device=dev),
+            stage_k=torch.empty(max(max(s.staging_kv for s in sts), 256), dtype=u8, device=dev),
+            hin_w=Pinned(max(s.inflow_w for s in sts)), hin_k=Pinned(max(s.inflow_kv for s in sts)),
+            hout_w=Pinned(max(s.outbound_w for s in sts)), hout_k=Pinned(max(s.outbound_kv for s in sts))))
     torch.cuda.synchronize()
 
     d = tempfile.mkdtemp(prefix="atp-", dir="/tmp")
@@ -562,17 +574,28 @@ def state_main(args):
         setup_ms = (time.perf_counter() - t0s) * 1e3
 
         def step():
-            recs = []
+            plans, recs = [], [None] * n_groups
+
+            def finish(j):
+                p = plans[j]
+                recs[j] = (p.sync(), [(x.kind, x.level, x.bytes, x.ms) for x in p.launches()])
+                plans[j] = None
+
             for i, g in enumerate(groups):
-                st = stats[g]
+                if i >= window:
+                    finish(i - window)  # its buffers serve this group
+                st, b = stats[g], slots[i % window]
                 (pw, wb), (pk, kb) = mapped[i]
                 p = built[g].plan()
-                p.reshard_weights(pw, wb, None, 0, hin_w.ptr, st.inflow_w, hout_w.ptr, st.outbound_w,
-                                  stage_w.data_ptr(), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
-                p.reshard_kv(pk, kb, None, 0, table_d.data_ptr(), shape[0], shape[1], hin_k.ptr,
-                             st.inflow_kv, hout_k.ptr, st.outbound_kv, stage_k.data_ptr(), stage_k.numel(),
-                             compute.cuda_stream, copy.cuda_stream)
-                recs.append((p.sync(), [(x.kind, x.level, x.bytes, x.ms) for x in p.launches()]))
+                p.reshard_weights(pw, wb, None, 0, b["hin_w"].ptr, st.inflow_w, b["hout_w"].ptr, st.outbound_w,
+                                  b["stage_w"].data_ptr(), b["stage_w"].numel(), compute.cuda_stream,
+                                  copy.cuda_stream)
+                p.reshard_kv(pk, kb, None, 0, table_d.data_ptr(), shape[0], shape[1], b["hin_k"].ptr,
+                             st.inflow_kv, b["hout_k"].ptr, st.outbound_kv, b["stage_k"].data_ptr(),
+                             b["stage_k"].numel(), compute.cuda_stream, copy.cuda_stream)
+                plans.append(p)
+            for j in range(max(0, n_groups - window), n_groups):
+                finish(j)
             return recs
 
         first_ms = None
@@ -642,7 +665,7 @@ def state_main(args):
                    "hidden": cfg["hidden"], "tp": f"{cfg['old_tp']}->{cfg['new_tp']}", "failed": cfg["failed"],
                    "self_old_rank": cfg["self_old"], "kv_sequences": cfg["n_seq"],
                    "seq_tokens": cfg["seq_tokens"], "in_place": True, "planner": "cm"},
-        "state": {"layer_groups": groups, "regions": len(regions),
+        "state": {"layer_groups": groups, "pending_at_once": window, "regions": len(regions),
                   "region_bytes": [b for _, b in regions], "region_limit": state.MAX_REGION,
                   "attach_ms": round(attach_ms, 3),
                   "setup_ms": round(setup_ms, 3),
