@@ -28,8 +28,13 @@
 namespace atp {
 namespace {
 
+// A failed call also stays the thread's last HIP error, which the caller's
+// next launch check (torch's, say) would report as its own: the error is
+// reported here, so it is cleared.
 void hip_check(hipError_t e, const char *what) {
-  if (e != hipSuccess) throw Error(ATP_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+  if (e == hipSuccess) return;
+  (void)hipGetLastError();
+  throw Error(ATP_EHIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 #define HIPCHK(x) hip_check((x), #x)
 

@@ -22,6 +22,8 @@ def _lib():
         _hip.hipHostMalloc.restype = C.c_int
         _hip.hipHostFree.argtypes = [C.c_void_p]
         _hip.hipHostFree.restype = C.c_int
+        _hip.hipGetLastError.argtypes = []
+        _hip.hipGetLastError.restype = C.c_int
     return _hip
 
 
@@ -31,6 +33,10 @@ class Pinned:
         p = C.c_void_p()
         rc = _lib().hipHostMalloc(C.byref(p), self.nbytes, 0)
         if rc != 0 or not p.value:
+            # a failed call also leaves its error as the thread's last HIP
+            # error, which torch's next kernel launch check would report as
+            # its own: clear it
+            _lib().hipGetLastError()
             raise MemoryError(f"hipHostMalloc({self.nbytes}) failed with HIP error {rc}")
         self.ptr = p.value
         arr = (C.c_uint8 * self.nbytes).from_address(self.ptr)
