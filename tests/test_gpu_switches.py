@@ -10,6 +10,8 @@
 * Fresh in-place plans one after another, with the earlier plans still
   alive (as a benchmark loop holds them), each choose the stream for the
   outbound work and stay bit-exact (outbound buffer included).
+* A refused pinned allocation leaves no HIP error behind for the next
+  kernel launch to report.
 """
 import numpy as np
 import pytest
@@ -209,3 +211,15 @@ def test_one_stream_for_compute_and_copy(flags):
     run_case(configs.get(1), flags=flags, one_stream=True, name=f"one-stream-flags{flags}")
     c = configs.scaled(2, layers=1, n_seq=2, seq_tokens=256)
     run_case(c, flags=flags, one_stream=True, name=f"one-stream-dense40-flags{flags}")
+
+
+def test_failed_pin_leaves_no_hip_error_behind():
+    """A pinned allocation the host refuses raises MemoryError, and the
+    next kernel launch (torch's fill here) does not report that stale
+    error as its own."""
+    from synth.pinned import Pinned
+    with pytest.raises(MemoryError):
+        Pinned(1 << 60)
+    x = torch.full((1 << 20,), 7, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    assert int(x[-1]) == 7
