@@ -772,6 +772,7 @@ int exec_sync(Plan &P, atp_timing *out) {
     for (hipEvent_t e : {cs.tail_compute, cs.tail_copy, cs.tail_side}) {
       if (!e) continue;
       hipError_t err = hipEventSynchronize(e);
+      if (err != hipSuccess) (void)hipGetLastError();  // reported below, as for hip_check
       if (err != hipSuccess && rc == ATP_OK) {
         rc = ATP_EHIP;
         msg = std::string("reshard failed on the GPU: ") + hipGetErrorString(err);
