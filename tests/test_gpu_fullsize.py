@@ -43,24 +43,53 @@ def _check(name, got, want, valid):
     assert bad.size == 0, f"{name}: {bad.size} of {valid.sum()} sampled words wrong"
 
 
-def _pin_all(sizes):
-    """Pin every host buffer of the reshard, (bytes, fill) each, before any
-    device memory is taken.  A host that cannot pin them all (about 69 GB
-    for the 80-layer workload) is a limit of the machine, not a result:
-    what was pinned is freed and the test is skipped."""
-    bufs = []
-    try:
-        for nbytes, f in sizes:
-            bufs.append(Pinned(nbytes, fill=f))
-    except MemoryError as e:
-        for b in bufs:
-            b.close()
-        bufs.clear()
-        pytest.skip(f"this host cannot pin {sum(x for x, _ in sizes) / 1e9:.1f} GB at once ({e})")
-    return bufs
+class _Pageable:
+    """Ordinary (pageable) host memory, 256-byte aligned, with the interface
+    of Pinned."""
+
+    def __init__(self, nbytes, fill=None):
+        self.nbytes = max(int(nbytes), 1)
+        self._raw = torch.empty(self.nbytes + 256, dtype=torch.uint8)
+        off = (-self._raw.data_ptr()) % 256
+        self.tensor = self._raw[off:off + self.nbytes]
+        self.ptr = self.tensor.data_ptr()
+        if fill is not None:
+            self.tensor.fill_(fill)
+
+    def close(self):
+        self.tensor = self._raw = None
 
 
-def run_full(n, inplace=None):
+def _pin_all(sizes, force_pageable=False):
+    """Host buffers of the reshard, (bytes, fill, dma_only) each, taken
+    before any device memory.  All are pinned if the host can pin them all
+    (about 69 GB for the 80-layer workload).  Otherwise the buffers that
+    only DMA copies read (the in-place KV inflow, which lands through the
+    landing ring; each of those copies waits only for work queued before
+    it) are taken as ordinary memory and the rest pinned.  A host that
+    cannot do even that is a limit of the machine, not a result: what was
+    taken is freed and the test is skipped."""
+    for pageable_dma in ((True,) if force_pageable else (False, True)):
+        if pageable_dma and not any(d for _, _, d in sizes):
+            break
+        bufs = []
+        try:
+            for nbytes, f, dma_only in sizes:
+                bufs.append((_Pageable if pageable_dma and dma_only else Pinned)(nbytes, fill=f))
+            if pageable_dma:
+                say(f"[fullsize] {sum(x for x, _, d in sizes if d) / 1e9:.1f} GB of DMA-only inflow "
+                    "in pageable memory")
+            return bufs
+        except MemoryError as e:
+            err = e
+            for b in bufs:
+                b.close()
+            bufs.clear()
+    pytest.skip(f"this host cannot pin {sum(x for x, _, d in sizes if not pageable_dma or not d) / 1e9:.1f} GB "
+                f"at once ({err})")
+
+
+def run_full(n, inplace=None, pageable_kv_inflow=False):
     c = configs.get(n, **({} if inplace is None else {"inplace": inplace}))
     pb = model.build(c)
     content = Content(c["seed"], c["w_kind"], c["kv_kind"])
@@ -72,8 +101,9 @@ def run_full(n, inplace=None):
     b = problem.build(c, n_live=len(live), pool=pool, flags=flags, staging_cap=c["staging_cap"] or 0)
     plan = b.plan()
     st = plan.stats()
-    hin_w, hin_k, hout_w, hout_k = _pin_all([(st.inflow_w, None), (st.inflow_kv, None),
-                                             (st.outbound_w, 0x3C), (st.outbound_kv, 0x3C)])
+    hin_w, hin_k, hout_w, hout_k = _pin_all([(st.inflow_w, None, False), (st.inflow_kv, None, inplace),
+                                             (st.outbound_w, 0x3C, False), (st.outbound_kv, 0x3C, False)],
+                                            force_pageable=pageable_kv_inflow)
     o_offs, o_size = pb.layout("old")
     n_offs, n_size = pb.layout("new")
     k_old, k_new = pb.kv_arena_bytes("old", pool), pb.kv_arena_bytes("new", pool)
@@ -117,7 +147,7 @@ def run_full(n, inplace=None):
     torch.cuda.synchronize()
     # ---- the reshard --------------------------------------------------------------
     compute, copy = torch.cuda.current_stream(), torch.cuda.Stream()
-    ptr = lambda t: None if t is None else (t.ptr if isinstance(t, Pinned) else t.data_ptr())
+    ptr = lambda t: None if t is None else (t.ptr if isinstance(t, (Pinned, _Pageable)) else t.data_ptr())
     plan.reshard_weights(ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0,
                          ptr(hin_w), st.inflow_w, ptr(hout_w), st.outbound_w if inplace else 0,
                          ptr(stage_w), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
@@ -172,3 +202,10 @@ def test_full_size_workload_2_in_place():
     """The headline shape resharded over its own old shard (what the state
     plane's regions hold)."""
     run_full(2, inplace=True)
+
+
+def test_full_size_workload_2_in_place_kv_inflow_pageable():
+    """In place the KV inflow lands through the landing ring by DMA only,
+    so it may sit in ordinary host memory (the fallback of hosts that
+    cannot pin every buffer of the 80-layer workload)."""
+    run_full(2, inplace=True, pageable_kv_inflow=True)
