@@ -191,6 +191,10 @@ int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes,
  * [n_seq][max_blocks], -1 = unused, read only; ids must be < num_blocks
  * and the distinct ids must number kv.live_blocks (else ATP_EINVAL from
  * atp_sync).  Buffers as for atp_reshard_weights, sizes from stats.*_kv.
+ * With ATP_INPLACE the KV inflow lands only by DMA through the landing
+ * ring (the copy kernel does not read it), so inflow_host may then be
+ * ordinary pageable memory, at a lower copy rate; the outbound buffer must
+ * still come from hipHostMalloc.
  * The weights and KV calls may be pending together if their staging
  * buffers do not overlap; with ATP_INPLACE the weights call must then come
  * first (a weights call after a pending KV call is ATP_ESTATE). */
