@@ -8,7 +8,9 @@ memory before the timed region.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N]
 
-Prints one JSON line.  `value` is the repack throughput in algorithmic
+The default workload is the largest: the dense 80-layer hidden-8192
+decoder, TP 8 -> 7, resharded in place under a 2 GB staging cap (about
+106 GB of HBM, 57 GB of inflow).  Prints one JSON line.  `value` is the repack throughput in algorithmic
 bytes (one read and one write of every retained byte that moves) per
 second of device repack time (the union of the repack kernels' intervals:
 the weights and KV repacks may overlap); `ms_per_step` is the wall time
@@ -27,13 +29,16 @@ import numpy as np
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 
-# HBM bytes per launch of the repack kernel measured with the FETCH_SIZE and
-# WRITE_SIZE counters (rocprofv3, one pass each, scaled by what the same
-# counters read for a plain 4 GiB copy: x2.0 and x1.0), valid only while the
-# kernel sources hash to `src`.
+# HBM bytes of the dominant repack launch (the one that moves the most
+# bytes) per workload, measured with the FETCH_SIZE and WRITE_SIZE counters
+# (rocprofv3, one pass each, scaled by what the same counters read for a
+# plain 4 GiB device copy: x2.0 and x1.0), keyed by call and the launch's
+# algorithmic bytes; valid only while the kernel sources hash to `src`.
 COUNTED_TRAFFIC = {
     "src": "98de88c3866af8ac",
-    "dense-40L-h5120-tp4to3": {"kv": 10738028373, "weights": 9069458016},
+    "dense-40L-h5120-tp4to3": {("kv", 10737418240): 10738045781, ("weights", 9043968000): 9069669589},
+    "dense-40L-h5120-tp8to7-fragmented-kv": {("kv", 21474836480): 21477139966},
+    "dense-80L-h8192-tp8to7-inplace": {("kv", 42949672960): 42954049916, ("weights", 3460300800): 3460448373},
 }
 
 
@@ -56,8 +61,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", type=int, default=2,
-                    help="1..5; 2 = dense 40L h5120 TP 4->3 (the headline workload)")
+    ap.add_argument("--workload", type=int, default=5,
+                    help="1..5; 5 = dense 80L h8192 TP 8->7 in place under a 2 GB staging cap (the "
+                         "largest workload, the default)")
     ap.add_argument("--plan", choices=["cm", "greedy", "full"], default="cm",
                     help="planner: CMM (Alg. 1) or the Greedy / Full Reload baselines of Sec. V")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -69,8 +75,11 @@ def parse():
                     help="also time the range-read reload source on a checkpoint written for this "
                          "workload: the reads alone (atp_load_weights), and reads and reshard pipelined "
                          "(atp_load_reshard_weights)")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="repeat the CPU oracle over the whole workload for at least this long")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="repeat each CPU oracle timing (one thread, then a thread pool) over its layer "
+                         "sample for at least this long")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="threads of the pooled CPU oracle timing (default: the host's CPUs, at most 16)")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="also run a plain device copy of this size (counter calibration)")
     ap.add_argument("--self-old", type=int, default=None,
@@ -104,7 +113,7 @@ def main():
     from paper_2511_11617_amd import atp, problem
     from synth import configs, fill, pagetable
     from synth.content import TAGS, Content
-    from synth.pinned import Pinned
+    from synth.pinned import Pageable, Pinned, host_buffers
 
     if args.state:
         return state_main(args)
@@ -178,13 +187,18 @@ def main():
         return (torch.empty(max(old_b, 256), dtype=u8, device=dev),
                 torch.empty(max(new_b, 256), dtype=u8, device=dev))
 
+    # host buffers first (pinning fails more often than device allocation);
+    # in place the KV inflow lands by DMA only and may be pageable memory
+    (hin_w, hin_k, hout_w, hout_k), pageable_bytes = host_buffers(
+        [(st.inflow_w, None, False), (st.inflow_kv, None, inplace),
+         (st.outbound_w if inplace else 1, None, False), (st.outbound_kv if inplace else 1, None, False)])
+    if pageable_bytes:
+        log(f"[bench] the host cannot pin every buffer: {pageable_bytes / 1e9:.1f} GB of KV inflow "
+            "(DMA only) in pageable memory")
     aw, nw = arena(st.old_arena_bytes, st.new_arena_bytes)
     ak, nk = arena(st.old_kv_bytes, st.new_kv_bytes)
     stage_w = torch.empty(max(st.staging_w, 256), dtype=u8, device=dev)
     stage_k = torch.empty(max(st.staging_kv, 256), dtype=u8, device=dev)
-    hin_w, hin_k = Pinned(st.inflow_w), Pinned(st.inflow_kv)
-    hout_w = Pinned(st.outbound_w if inplace else 1)
-    hout_k = Pinned(st.outbound_kv if inplace else 1)
     table_d = torch.from_numpy(table).to(dev)
 
     # ---- synthetic content -----------------------------------------------------
@@ -222,7 +236,7 @@ def main():
     copy = torch.cuda.Stream()
     h2d_peak = h2d_probe(torch, [hin_w, hin_k], max(st.inflow_w, st.inflow_kv), copy)
     log(f"[bench] standalone H2D of the inflow buffers: {h2d_peak:.1f} GB/s")
-    ptr = lambda t: None if t is None else (t.ptr if isinstance(t, Pinned) else t.data_ptr())
+    ptr = lambda t: None if t is None else (t.ptr if isinstance(t, (Pinned, Pageable)) else t.data_ptr())
 
     issue = []  # host time spent enqueuing each call (ms)
     # the first reshard's one-time set-up, done ahead of it (a recovering
@@ -301,8 +315,9 @@ def main():
     dk, db, dom_ms, dom_gbps, kernels = dominant_launch(launches)
     traffic = None
     counted = COUNTED_TRAFFIC.get(cfg["name"])
-    if counted and args.plan == "cm" and not args.inplace and kernel_src_hash() == COUNTED_TRAFFIC["src"]:
-        traffic = counted.get("weights" if dk == 0 else "kv")
+    if counted and args.plan == "cm" and not args.inplace and args.kv_budget is None \
+            and kernel_src_hash() == COUNTED_TRAFFIC["src"]:
+        traffic = counted.get(("weights" if dk == 0 else "kv", 2 * db))
 
     out = {
         "metric": "reshard GB/s (fraction of HBM peak) + wall ms per TP k→k-1; reload bytes vs min",
@@ -335,6 +350,7 @@ def main():
         "h2d_GBps_pcie_inclusive": round((st.inflow_w + st.inflow_kv) / (h2d_ms * 1e-3) / 1e9, 2)
         if h2d_ms else None,
         "h2d_standalone_GBps": round(h2d_peak, 2),
+        "host_pageable_bytes": int(pageable_bytes),
         "wall_vs_h2d_bound": round((st.inflow_w + st.inflow_kv) / (h2d_peak * 1e9) * 1e3 / wall_ms, 3)
         if h2d_peak else None,
         "overlap": round(sum(t.overlap for t in recs) / K, 3),
@@ -385,8 +401,8 @@ def main():
         if inplace:
             fill_old()
             torch.cuda.synchronize()
-        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, aw, ak, hin_w.tensor, hin_k.tensor,
-                                           table, pool)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, args.cpu_threads, aw, ak, hin_w.tensor,
+                                           hin_k.tensor, table, pool)
     print(json.dumps(out), flush=True)
 
 
@@ -792,31 +808,68 @@ def h2d_probe(torch, bufs, max_bytes, stream, chunk=64 << 20):
     return tot / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline(cfg, seconds, aw, ak, hin_w, hin_k, table, pool):
+def cpu_baseline(cfg, seconds, threads, aw, ak, hin_w, hin_k, table, pool):
     """The oracle's plan execution (old shard + packed inflow -> new shard,
-    numpy slicing on one host thread) over the whole workload, repeated
-    until `seconds` have passed (at most 8 passes)."""
+    host to host) on a sample of the workload's layers.
+
+    Every layer has the same plan, and the weight arena, the KV planes and
+    both packed inflow buffers are layer-major, so the buffers of the first
+    n layers are those of the same decoder with n layers.  Timed twice over
+    the same sample: the oracle on one thread (one call for the weights, one
+    for the KV cache), then a pool of threads, one task per (layer, weights or
+    KV) on the one-layer problem.  NumPy releases the GIL in its copies."""
+    from concurrent.futures import ThreadPoolExecutor
+
     from oracle import model, repack
 
-    pb = model.build(cfg)
-    _, o_size = pb.layout("old")
-    kv_old = pb.kv_arena_bytes("old", pool)
+    threads = threads or min(os.cpu_count() or 1, 16)
+    L = cfg["layers"]
+    n = min(L, max(threads, 4))
     n_live = len(repack.live_blocks(table))
-    old_w = aw[:o_size].cpu().numpy()
-    old_k = ak[:kv_old].cpu().numpy()
-    ret, inf, _ = repack.self_bytes(pb, n_live)
-    in_w = hin_w.numpy()[:sum(s[-1] for s in repack.inflow_segments(pb, n_live)[0])]
-    in_k = hin_k.numpy()[:sum(s[-1] for s in repack.inflow_segments(pb, n_live)[1])]
-    passes, t0 = 0, time.perf_counter()
-    while passes < 8 and (passes == 0 or time.perf_counter() - t0 < seconds):
-        repack.apply_weights(pb, old_w, in_w)
-        repack.apply_kv(pb, old_k, in_k, table, pool)
-        passes += 1
-    dt = (time.perf_counter() - t0) / passes
-    return {"value": round(2 * ret / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"whole workload ({cfg['layers']} layers, weights + KV, "
-                      f"{2 * ret / 1e9:.2f} GB algorithmic repack + {inf / 1e9:.2f} GB inflow placed), "
-                      f"{passes} passes, {dt:.2f} s per pass, numpy on one thread"}
+    pb1 = model.build(dict(cfg, layers=1))
+    pbn = model.build(dict(cfg, layers=n))
+    w_stride, kv_stride = pb1.layout("old")[1], pb1.kv_arena_bytes("old", pool)
+    win1 = sum(s[-1] for s in repack.inflow_segments(pb1, n_live)[0])
+    kin1 = sum(s[-1] for s in repack.inflow_segments(pb1, n_live)[1])
+    old_w = aw[:n * w_stride].cpu().numpy()
+    old_k = ak[:n * kv_stride].cpu().numpy()
+    in_w = hin_w.numpy()[:n * win1]
+    in_k = hin_k.numpy()[:n * kin1]
+    ret1, inf1, _ = repack.self_bytes(pb1, n_live)
+    alg = 2 * ret1 * n
+
+    def timed(one_pass):
+        passes, t0 = 0, time.perf_counter()
+        while passes < 8 and (passes == 0 or time.perf_counter() - t0 < seconds):
+            one_pass()
+            passes += 1
+        return (time.perf_counter() - t0) / passes, passes
+
+    def serial():
+        repack.apply_weights(pbn, old_w, in_w)
+        repack.apply_kv(pbn, old_k, in_k, table, pool)
+
+    tasks = [(l, part) for l in range(n) for part in ("weights", "kv")]
+
+    def one(task):
+        l, part = task
+        if part == "weights":
+            repack.apply_weights(pb1, old_w[l * w_stride:(l + 1) * w_stride], in_w[l * win1:(l + 1) * win1])
+        else:
+            repack.apply_kv(pb1, old_k[l * kv_stride:(l + 1) * kv_stride], in_k[l * kin1:(l + 1) * kin1],
+                            table, pool)
+
+    dt1, p1 = timed(serial)
+    with ThreadPoolExecutor(threads) as ex:
+        dtn, pn = timed(lambda: list(ex.map(one, tasks)))
+    sample = (f"{n} of {L} layers (weights + KV: {alg / 1e9:.2f} GB algorithmic repack + "
+              f"{inf1 * n / 1e9:.2f} GB inflow placed), host to host")
+    return {"value": round(alg / dtn / 1e9, 3), "unit": "GB/s", "cores": threads, "threads": threads,
+            "kind": "oracle", "host_cpus": os.cpu_count(),
+            "sample": sample + f"; {threads} threads over (layer, weights|KV), {pn} passes of {dtn:.2f} s",
+            "single_thread": {"value": round(alg / dt1 / 1e9, 3), "unit": "GB/s", "cores": 1,
+                              "passes": p1, "s_per_pass": round(dt1, 3)},
+            "threaded_s_per_pass": round(dtn, 3)}
 
 
 if __name__ == "__main__":

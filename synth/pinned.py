@@ -55,3 +55,47 @@ class Pinned:
             self.close()
         except Exception:
             pass
+
+
+class Pageable:
+    """Ordinary (pageable) host memory, 256-byte aligned, with the interface
+    of Pinned."""
+
+    def __init__(self, nbytes: int, fill: int | None = None):
+        self.nbytes = max(int(nbytes), 1)
+        self._raw = torch.empty(self.nbytes + 256, dtype=torch.uint8)
+        off = (-self._raw.data_ptr()) % 256
+        self.tensor = self._raw[off:off + self.nbytes]
+        self.ptr = self.tensor.data_ptr()
+        if fill is not None:
+            self.tensor.fill_(fill)
+
+    def close(self):
+        self.tensor = self._raw = None
+
+
+def host_buffers(sizes, force_pageable: bool = False):
+    """Host buffers of one reshard, from `sizes` = [(bytes, fill, dma_only)].
+
+    Every buffer is pinned if the host can pin them all at once (about 69 GB
+    for the 80-layer TP 8->7 share).  Otherwise the buffers that only DMA
+    copies touch (`dma_only`: the in-place KV inflow, which lands through the
+    landing ring) are taken as ordinary memory and the rest pinned; the copy
+    kernel itself reads or writes the others, so they must be pinned.
+    Returns (buffers, pageable bytes); raises MemoryError, having freed what
+    it took, when even that fails."""
+    err = None
+    for pageable_dma in ((True,) if force_pageable else (False, True)):
+        if pageable_dma and not any(d for _, _, d in sizes):
+            break
+        bufs = []
+        try:
+            for nbytes, f, dma_only in sizes:
+                bufs.append((Pageable if pageable_dma and dma_only else Pinned)(nbytes, fill=f))
+            return bufs, sum(int(n) for n, _, d in sizes if d) if pageable_dma else 0
+        except MemoryError as e:
+            err = e
+            for b in bufs:
+                b.close()
+    need = sum(int(n) for n, _, d in sizes if not (force_pageable and d))
+    raise MemoryError(f"this host cannot pin the reshard's host buffers ({need / 1e9:.1f} GB): {err}")

@@ -15,7 +15,7 @@ import torch
 from oracle import model, repack
 from paper_2511_11617_amd import atp, problem
 from synth import configs, fill, pagetable
-from synth.pinned import Pinned
+from synth.pinned import Pageable, Pinned, host_buffers
 from synth.content import Content
 from tests.gpu_harness import say
 
@@ -43,50 +43,18 @@ def _check(name, got, want, valid):
     assert bad.size == 0, f"{name}: {bad.size} of {valid.sum()} sampled words wrong"
 
 
-class _Pageable:
-    """Ordinary (pageable) host memory, 256-byte aligned, with the interface
-    of Pinned."""
-
-    def __init__(self, nbytes, fill=None):
-        self.nbytes = max(int(nbytes), 1)
-        self._raw = torch.empty(self.nbytes + 256, dtype=torch.uint8)
-        off = (-self._raw.data_ptr()) % 256
-        self.tensor = self._raw[off:off + self.nbytes]
-        self.ptr = self.tensor.data_ptr()
-        if fill is not None:
-            self.tensor.fill_(fill)
-
-    def close(self):
-        self.tensor = self._raw = None
-
-
 def _pin_all(sizes, force_pageable=False):
-    """Host buffers of the reshard, (bytes, fill, dma_only) each, taken
-    before any device memory.  All are pinned if the host can pin them all
-    (about 69 GB for the 80-layer workload).  Otherwise the buffers that
-    only DMA copies read (the in-place KV inflow, which lands through the
-    landing ring; each of those copies waits only for work queued before
-    it) are taken as ordinary memory and the rest pinned.  A host that
-    cannot do even that is a limit of the machine, not a result: what was
-    taken is freed and the test is skipped."""
-    for pageable_dma in ((True,) if force_pageable else (False, True)):
-        if pageable_dma and not any(d for _, _, d in sizes):
-            break
-        bufs = []
-        try:
-            for nbytes, f, dma_only in sizes:
-                bufs.append((_Pageable if pageable_dma and dma_only else Pinned)(nbytes, fill=f))
-            if pageable_dma:
-                say(f"[fullsize] {sum(x for x, _, d in sizes if d) / 1e9:.1f} GB of DMA-only inflow "
-                    "in pageable memory")
-            return bufs
-        except MemoryError as e:
-            err = e
-            for b in bufs:
-                b.close()
-            bufs.clear()
-    pytest.skip(f"this host cannot pin {sum(x for x, _, d in sizes if not pageable_dma or not d) / 1e9:.1f} GB "
-                f"at once ({err})")
+    """Host buffers of the reshard, taken before any device memory (see
+    synth.pinned.host_buffers).  A host that cannot pin even the buffers the
+    copy kernel touches is a limit of the machine, not a result: the test is
+    skipped, naming the size."""
+    try:
+        bufs, pageable = host_buffers(sizes, force_pageable)
+    except MemoryError as e:
+        pytest.skip(str(e))
+    if pageable:
+        say(f"[fullsize] {pageable / 1e9:.1f} GB of DMA-only inflow in pageable memory")
+    return bufs
 
 
 def run_full(n, inplace=None, pageable_kv_inflow=False):
@@ -147,7 +115,7 @@ def run_full(n, inplace=None, pageable_kv_inflow=False):
     torch.cuda.synchronize()
     # ---- the reshard --------------------------------------------------------------
     compute, copy = torch.cuda.current_stream(), torch.cuda.Stream()
-    ptr = lambda t: None if t is None else (t.ptr if isinstance(t, (Pinned, _Pageable)) else t.data_ptr())
+    ptr = lambda t: None if t is None else (t.ptr if isinstance(t, (Pinned, Pageable)) else t.data_ptr())
     plan.reshard_weights(ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0,
                          ptr(hin_w), st.inflow_w, ptr(hout_w), st.outbound_w if inplace else 0,
                          ptr(stage_w), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
