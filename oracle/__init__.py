@@ -14,9 +14,14 @@ Modules
   repack   the new shard by definition (slicing the full tensors) and by
            executing the oracle's own plan (old shard + packed inflow).
   brute    exhaustive searches used to pin the plan on tiny inputs.
-  hazard   replays an in-place copy schedule on a shadow copy of the arena.
+  kvbudget the least-recently-used session eviction of the KV budget.
 
-Every function is pinned by CPU tests (tests/test_oracle_*.py) to the
-paper's worked example (Fig. 3), hand-computed shard splits, Eq. 1's closed
-form, brute force and invariants; nothing is "parity unpinned".
+Every function is pinned by CPU tests (tests/test_oracle_*.py,
+tests/test_kv_budget.py) to something other than itself: the paper's worked
+example (Fig. 3), hand-computed shard splits and hand-located words of the
+tiny workload (tests/golden/), Eq. 1's closed form, brute force, and
+invariants (every target's new shards and KV blocks together rebuild the
+full tensors; outbound bytes are what the receiving peers' new shards hold).
+tests/test_oracle_mutants.py plants one-line index mistakes in the oracle
+and requires a pin to fail on each.
 """

@@ -220,13 +220,19 @@ def test_assignment_bruteforce():
 
 def test_inorder_not_always_optimal():
     """Reading check: in-order hosting can keep fewer bytes than the best
-    permutation (4 -> 3, old rank 3 fails, 14/13/13 query-head split)."""
+    permutation.  4 -> 3 with old rank 3 failed: on the query heads alone
+    (14/13/13) both keep 19 heads, but over every space in bytes (query heads,
+    KV heads 3/3/2 with their cache, FFN units) in-order keeps strictly less
+    (tests/test_oracle_pins.py counts the bytes from the shapes)."""
     old = cmm.even_ranges(40, 4)
     targets = cmm.ranges_from_widths([14, 13, 13])
     failed = [3]
     inorder = cmm.assign_inorder(4, failed, 3)
     mr = cmm.assign_maxretain(4, failed, 3, {"q": old}, {"q": targets}, {"q": 1})
-    assert brute.unit_retained(old, mr, targets) >= brute.unit_retained(old, inorder, targets)
+    assert brute.unit_retained(old, mr, targets) == brute.unit_retained(old, inorder, targets) == 19
+    from tests.test_oracle_pins import pin_inorder_strict
+    inorder_bytes, best_bytes = pin_inorder_strict()
+    assert inorder_bytes < best_bytes
 
 
 # --------------------------------------------------------------------------
