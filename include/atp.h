@@ -56,30 +56,39 @@ typedef struct {
 } atp_range;
 
 /* ---- partition spaces (Sec. III-B, Alg. 1) ------------------------------ */
-/* How the new ranges of a space are obtained.
- *   EXPLICIT    new_ranges given by the caller (M ranges, in target order)
- *   FLOOR       Alg. 1: target j = [floor(j H / M), floor((j+1) H / M))
- *   CEIL_FIRST  Sec. III-B widths ceil(H/M) first, then floor(H/M)
- *   GQA         ranges follow another (query-head) space's new ranges:
- *               query heads [a, b) need KV heads [floor(a/g), ceil(b/g))
- *               with g = gqa_group; ranges may overlap (replicas). */
-enum { ATP_RULE_EXPLICIT = 0, ATP_RULE_FLOOR = 1, ATP_RULE_CEIL_FIRST = 2, ATP_RULE_GQA = 3 };
+/* How the old ranges (old_tp of them) or the new ranges (new_tp of them,
+ * one per target, in target order) of a space are obtained; n is old_tp or
+ * new_tp.
+ *   EXPLICIT    given by the caller (old_ranges / new_ranges)
+ *   FLOOR       Alg. 1: range j = [floor(j H / n), floor((j+1) H / n))
+ *   CEIL_FIRST  Sec. III-B unequal widths: ceil(H/n) wide first, then
+ *               floor(H/n) (the even split when n divides H)
+ *   GQA         ranges follow the query-head space `gqa_space` (old ranges
+ *               its old ranges, new ranges its new ones): query heads
+ *               [a, b) need KV heads [floor(a/g), ceil(b/g)) with
+ *               g = gqa_group; ranges may overlap (replicas)
+ *   WIDTHS      consecutive ranges of the given widths (old_widths /
+ *               new_widths), which must add up to H */
+enum { ATP_RULE_EXPLICIT = 0, ATP_RULE_FLOOR = 1, ATP_RULE_CEIL_FIRST = 2, ATP_RULE_GQA = 3,
+       ATP_RULE_WIDTHS = 4 };
 
 /* One space: attention heads, KV heads, FFN column groups, experts.
  * total_units is H; with Alg. 1 it is the largest end of any old range,
- * dead ranks included.  old_ranges[i] is old rank i's range (N = old_tp of
- * them, dead ranks included); they may overlap (replicated units) and must
- * together cover [0, H). */
+ * dead ranks included.  Old rank i's range (dead ranks included) comes
+ * from old_rule; the old ranges may overlap (replicated units) and must
+ * together cover [0, H), and so must the new ranges. */
 typedef struct {
   int64_t total_units;
   int32_t old_tp;
   int32_t new_tp;
-  const atp_range *old_ranges;
+  const atp_range *old_ranges; /* old_rule EXPLICIT: old_tp ranges   */
   int32_t new_rule;
   int32_t gqa_space; /* GQA: index of the query-head space     */
   int32_t gqa_group; /* GQA: query heads per KV head           */
-  int32_t reserved;
-  const atp_range *new_ranges; /* EXPLICIT: new_tp ranges         */
+  int32_t old_rule;  /* ATP_RULE_*; 0 = EXPLICIT (old_ranges)  */
+  const atp_range *new_ranges; /* new_rule EXPLICIT: new_tp ranges   */
+  const int64_t *old_widths;   /* old_rule WIDTHS: old_tp widths     */
+  const int64_t *new_widths;   /* new_rule WIDTHS: new_tp widths     */
 } atp_space;
 
 /* ---- tensors (Sec. III-B layout invariants) ----------------------------- */
@@ -229,9 +238,17 @@ typedef struct {
                              KV repacks overlap                          */
 } atp_timing;
 
-/* Wait for the pending reshard calls of `plan`; returns the first
- * asynchronous error (ATP_EINVAL for a bad block table, ATP_EHIP).
- * `out` may be NULL. */
+/* Wait for the pending reshard calls of `plan` and report them.  This ends
+ * the reshard's freeze window (Sec. III-B: serving pauses while parameters
+ * and KV are re-laid out, then resumes on the new layout): when it returns
+ * ATP_OK, every retained byte is in its new place and every inflow byte has
+ * landed (Sec. III-C: the reloads and transfers that were pipelined with the
+ * repack are complete), so the caller may switch its views to the new
+ * layout, reuse the host buffers and free staging.  Returns the first
+ * asynchronous error: ATP_EINVAL for a bad block table (an id >= num_blocks,
+ * or a live-block count other than kv.live_blocks), ATP_EHIP for a failure
+ * on the GPU; ATP_ESTATE if nothing was issued.  Whatever it returns, no
+ * work of the plan is still running afterwards.  `out` may be NULL. */
 int atp_sync(atp_plan_t *plan, atp_timing *out);
 
 /* Optional: do, before the first reshard on the current device, the
@@ -279,6 +296,9 @@ int atp_plan_tasks(const atp_plan_t *plan, int32_t space, atp_task *out,
 /* Resolved new ranges of one space, in target order. */
 int atp_plan_ranges(const atp_plan_t *plan, int32_t space, atp_range *out,
                     int32_t cap, int32_t *n);
+/* Resolved old ranges of one space, in old-rank order (dead ranks included). */
+int atp_plan_old_ranges(const atp_plan_t *plan, int32_t space, atp_range *out,
+                        int32_t cap, int32_t *n);
 /* owner[j] = old rank hosting target j. */
 int atp_plan_owner(const atp_plan_t *plan, int32_t *owner, int32_t cap, int32_t *n);
 /* Old/new byte offsets and new shard bytes of tensor `t`. */

@@ -18,7 +18,7 @@ LIB_PATH = os.environ.get("ATP_LIB") or os.path.join(_HERE, "libatp.so")
 
 # ---- status codes and enums (atp.h) -----------------------------------------
 OK, EINVAL, ECAPACITY, EHIP, EALIGN, ESTATE = 0, -1, -2, -3, -4, -5
-RULE_EXPLICIT, RULE_FLOOR, RULE_CEIL_FIRST, RULE_GQA = 0, 1, 2, 3
+RULE_EXPLICIT, RULE_FLOOR, RULE_CEIL_FIRST, RULE_GQA, RULE_WIDTHS = 0, 1, 2, 3, 4
 ROWS, COLS = 0, 1
 OFFSET_AUTO = (1 << 64) - 1
 KV_HEAD_MAJOR, KV_TOKEN_MAJOR = 0, 1
@@ -32,7 +32,7 @@ SEG_INFLOW_W, SEG_OUTBOUND_W, SEG_INFLOW_KV, SEG_OUTBOUND_KV = 0, 1, 2, 3
 
 EXPORTS = [
     "atp_plan", "atp_plan_free", "atp_reshard_weights", "atp_reshard_kv", "atp_sync",
-    "atp_plan_stats", "atp_plan_tasks", "atp_plan_ranges", "atp_plan_owner",
+    "atp_plan_stats", "atp_plan_tasks", "atp_plan_ranges", "atp_plan_old_ranges", "atp_plan_owner",
     "atp_plan_layout", "atp_plan_segments", "atp_plan_launches", "atp_partition",
     "atp_last_error", "atp_st_open", "atp_st_close", "atp_st_find", "atp_load_weights",
     "atp_kv_evict_lru", "atp_daemon_serve", "atp_state_connect", "atp_state_disconnect",
@@ -48,8 +48,9 @@ class Range(C.Structure):
 class Space(C.Structure):
     _fields_ = [("total_units", C.c_int64), ("old_tp", C.c_int32), ("new_tp", C.c_int32),
                 ("old_ranges", C.POINTER(Range)), ("new_rule", C.c_int32),
-                ("gqa_space", C.c_int32), ("gqa_group", C.c_int32), ("reserved", C.c_int32),
-                ("new_ranges", C.POINTER(Range))]
+                ("gqa_space", C.c_int32), ("gqa_group", C.c_int32), ("old_rule", C.c_int32),
+                ("new_ranges", C.POINTER(Range)), ("old_widths", C.POINTER(C.c_int64)),
+                ("new_widths", C.POINTER(C.c_int64))]
 
 
 class Tensor(C.Structure):
@@ -158,6 +159,7 @@ def _load():
     lib.atp_plan_stats.argtypes = [P, C.POINTER(Stats)]
     lib.atp_plan_tasks.argtypes = [P, C.c_int32, C.POINTER(Task), C.c_int32, C.POINTER(C.c_int32)]
     lib.atp_plan_ranges.argtypes = [P, C.c_int32, C.POINTER(Range), C.c_int32, C.POINTER(C.c_int32)]
+    lib.atp_plan_old_ranges.argtypes = [P, C.c_int32, C.POINTER(Range), C.c_int32, C.POINTER(C.c_int32)]
     lib.atp_plan_owner.argtypes = [P, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32)]
     lib.atp_plan_layout.argtypes = [P, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                                     C.POINTER(C.c_uint64)]
@@ -261,6 +263,9 @@ class Plan:
 
     def ranges(self, space: int):
         return [(r.begin, r.end) for r in _list(lib.atp_plan_ranges, self.h, Range, space)]
+
+    def old_ranges(self, space: int):
+        return [(r.begin, r.end) for r in _list(lib.atp_plan_old_ranges, self.h, Range, space)]
 
     def owner(self):
         return [int(x) for x in _list(lib.atp_plan_owner, self.h, C.c_int32)]

@@ -144,6 +144,14 @@ int atp_plan_ranges(const atp_plan_t *plan, int32_t space, atp_range *out, int32
   return copy_out(r, out, cap, n);
 }
 
+int atp_plan_old_ranges(const atp_plan_t *plan, int32_t space, atp_range *out, int32_t cap, int32_t *n) {
+  if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+  if (space < 0 || space >= int32_t(plan->p->sp.size())) return fail(ATP_EINVAL, "bad space");
+  std::vector<atp_range> r;
+  for (const atp::Rng &x : plan->p->sp[space].old_r) r.push_back({x.b, x.e});
+  return copy_out(r, out, cap, n);
+}
+
 int atp_plan_owner(const atp_plan_t *plan, int32_t *owner, int32_t cap, int32_t *n) {
   if (!plan) return fail(ATP_EINVAL, "plan is NULL");
   std::vector<int32_t> o(plan->p->owner.begin(), plan->p->owner.end());

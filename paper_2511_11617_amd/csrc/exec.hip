@@ -44,8 +44,15 @@ uint64_t magic_of(uint64_t d) {
   return uint64_t(m);
 }
 
+// A half-open byte range of device memory a call touches.
+struct Span {
+  uintptr_t b = 0, e = 0;
+  bool meets(const Span &o) const { return b < e && o.b < o.e && b < o.e && o.b < e; }
+};
+
 struct CallState {
   bool pending = false;
+  Span old_arena, new_arena, staging;  // what the pending call reads and writes
   Desc *desc_host = nullptr;  // pinned copy of the descriptors
   size_t desc_cap = 0;
   int32_t *err_host = nullptr;  // pinned error word
@@ -128,13 +135,15 @@ struct Exec {
     {
       std::lock_guard<std::mutex> g(g_pool_mu);
       auto &v = g_pools[device].pinned;
+      size_t best = v.size();  // the smallest pooled buffer that fits
       for (size_t i = 0; i < v.size(); ++i)
-        if (v[i].second >= bytes) {
-          void *p = v[i].first;
-          *cap = v[i].second;
-          v.erase(v.begin() + long(i));
-          return p;
-        }
+        if (v[i].second >= bytes && (best == v.size() || v[i].second < v[best].second)) best = i;
+      if (best < v.size()) {
+        void *p = v[best].first;
+        *cap = v[best].second;
+        v.erase(v.begin() + long(best));
+        return p;
+      }
     }
     void *p = nullptr;
     HIPCHK(hipHostMalloc(&p, bytes, hipHostMallocDefault));
@@ -421,13 +430,14 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
                const int32_t *table, int64_t n_entries, void *staging, uint64_t staging_bytes, hipStream_t compute,
                hipStream_t copy, const std::function<void(uint64_t)> *await) {
   CallPlan &c = kvcall ? P.k : P.w;
-  Exec &E = exec_of(P);
-  CallState &cs = kvcall ? E.k : E.w;
-  if (cs.pending) throw Error(ATP_ESTATE, "reshard called again before atp_sync");
+  // Every argument is checked before the first HIP call.  The executor's
+  // state exists from the plan's first call on; before it nothing is pending.
+  Exec *Ep = static_cast<Exec *>(P.exec);
+  if (Ep && (kvcall ? Ep->k : Ep->w).pending) throw Error(ATP_ESTATE, "reshard called again before atp_sync");
   // In place, a weights call issued while the KV call is pending ended one
   // process with a host fault whose cause is not known; that order is
   // refused until it is.
-  if (P.inplace && !kvcall && E.k.pending)
+  if (P.inplace && !kvcall && Ep && Ep->k.pending)
     throw Error(ATP_ESTATE, "in place, call atp_reshard_weights before atp_reshard_kv (or after atp_sync)");
   const char *what = kvcall ? "kv" : "weights";
   // ---- argument checks ------------------------------------------------------
@@ -460,8 +470,32 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   if (kvcall && (!table || n_entries <= 0)) throw Error(ATP_EINVAL, "kv: block table missing");
   check_extents(c, kvcall, P, P.inplace ? arena_bytes : c.old_bytes, P.inplace ? arena_bytes : new_bytes,
                 staging_bytes, inflow_bytes, do_out ? outbound_bytes : 0);
+  // Device memory this call touches: the arenas (in place one span of the
+  // larger layout) and the part of staging it uses for descriptors, prefix
+  // sums, block lists, the landing ring and staged pieces.  Staging may not
+  // meet an arena, and neither may meet what a pending call of the other
+  // kind touches (both would write there while the other still reads).
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(arena), n0 = reinterpret_cast<uintptr_t>(new_arena),
+                  s0 = reinterpret_cast<uintptr_t>(staging);
+  Span my_old{a0, a0 + (P.inplace ? std::max(c.old_bytes, c.new_bytes) : c.old_bytes)};
+  Span my_new = P.inplace ? Span{} : Span{n0, n0 + c.new_bytes};
+  Span my_st{s0, s0 + c.staging_need};
+  if (my_st.meets(my_old) || my_st.meets(my_new))
+    throw Error(ATP_EINVAL, std::string(what) + ": staging overlaps an arena");
+  if (Ep) {
+    const CallState &o = kvcall ? Ep->w : Ep->k;
+    if (o.pending)
+      for (const Span &mine : {my_old, my_new, my_st})
+        for (const Span &theirs : {o.old_arena, o.new_arena, o.staging})
+          if (mine.meets(theirs))
+            throw Error(ATP_EINVAL, std::string(what) + ": an arena or staging buffer overlaps one of the pending " +
+                                        (kvcall ? "weights" : "kv") + " call");
+  }
   if (!c.host_reads.empty()) check_kernel_host_buffer(inflow_host, inflow_bytes, "inflow buffer");
   if (do_out && c.out_d0 >= 0) check_kernel_host_buffer(outbound_host, c.outbound_bytes, "outbound buffer");
+
+  Exec &E = exec_of(P);
+  CallState &cs = kvcall ? E.k : E.w;
 
   int dev = -1;
   HIPCHK(hipGetDevice(&dev));
@@ -476,6 +510,9 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     cs.err_host = static_cast<int32_t *>(E.pinned(256, &cap));
   }
   *cs.err_host = 0;
+  cs.old_arena = my_old;
+  cs.new_arena = my_new;
+  cs.staging = my_st;
   cs.launches.clear();
   cs.h2d_bytes = cs.d2h_bytes = cs.scatter_bytes = cs.repack_bytes = 0;
   build_descs(E, c, cs);
@@ -498,29 +535,26 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   const bool use_side = do_out || early_reads;
   if (use_side) choose_side(E, compute, copy);
 
-  // every stream starts after what the caller already queued on `compute`
-  // The other call of a weights + KV pair may already be pending: its
-  // start event marks the caller's prior work, so this call's landings
-  // need not wait for that call's own kernels.
-  CallState &other = kvcall ? E.w : E.k;
-  hipEvent_t start = other.pending && other.start ? other.start : nullptr;
-  if (!start) {
-    start = E.ev_sync();
-    HIPCHK(hipEventRecord(start, compute));
-  }
-  cs.start = start;
-  HIPCHK(hipStreamWaitEvent(copy, start, 0));
+  // every stream of this call starts after what the caller has queued on
+  // `compute` when the call is made (with the other call of the plan
+  // pending, that includes the other call's work on `compute`)
+  cs.start = E.ev_sync();
+  HIPCHK(hipEventRecord(cs.start, compute));
+  HIPCHK(hipStreamWaitEvent(copy, cs.start, 0));
 
   // direct landings wait for nothing (the planner routes every landing that
   // would wait for a level or an outbound read elsewhere): they go first, so
-  // that the link is busy at once
+  // that the link is busy at once.  While the inflow buffer is still being
+  // filled (`await`) they go after the levels instead, with the host reads,
+  // so that the host does not wait for the reads before the repack is queued.
   cs.h2d0 = E.ev_time();
   HIPCHK(hipEventRecord(cs.h2d0, copy));
-  for (const HostCopy &h : c.directs) {
-    if (await) (*await)(h.host_off + h.bytes);
+  auto issue_direct = [&](const HostCopy &h) {
     HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
     cs.h2d_bytes += h.bytes;
-  }
+  };
+  if (!await)
+    for (const HostCopy &h : c.directs) issue_direct(h);
 
   // ---- upload descriptors, prepare ----------------------------------------------
   if (!c.fams.empty())
@@ -550,25 +584,33 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   }
 
   // the copy kernel reads inflow pieces from the pinned host buffer into
-  // their final place (kind 4 launches).  While the inflow buffer is still
-  // being filled (`await`), each launch is cut at descriptor boundaries into
-  // pieces of at least kPipeBytes, each issued once the bytes it reads are in.
-  auto issue_host_reads = [&](hipStream_t s) {
-    auto one = [&](const Launch &L) {
-      CallState::LaunchRec r{4, -1, L.bytes, E.ev_time(), E.ev_time()};
-      HIPCHK(hipEventRecord(r.e0, s));
-      launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s,
-                  kHostReadGrid);
-      HIPCHK(hipEventRecord(r.e1, s));
-      cs.launches.push_back(r);
-      cs.h2d_bytes += L.bytes;
+  // their final place (kind 4 launches)
+  auto host_read = [&](const Launch &L, hipStream_t s) {
+    CallState::LaunchRec r{4, -1, L.bytes, E.ev_time(), E.ev_time()};
+    HIPCHK(hipEventRecord(r.e0, s));
+    launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s, kHostReadGrid);
+    HIPCHK(hipEventRecord(r.e1, s));
+    cs.launches.push_back(r);
+    cs.h2d_bytes += L.bytes;
+  };
+  auto end_host_reads = [&](hipStream_t s) {
+    cs.hr1 = E.ev_time();
+    HIPCHK(hipEventRecord(cs.hr1, s));
+  };
+  // While the inflow buffer is still being filled (`await`), the direct
+  // landings and the host reads (each launch cut at descriptor boundaries
+  // into pieces of at least kPipeBytes) are issued in the order of the end
+  // of the bytes they read, each once those bytes are in.
+  auto issue_awaited = [&](hipStream_t s) {
+    struct Piece {
+      uint64_t end;
+      const HostCopy *direct;
+      Launch L;
     };
+    std::vector<Piece> pieces;
+    for (const HostCopy &h : c.directs) pieces.push_back({h.host_off + h.bytes, &h, Launch{}});
     const int64_t nb = kvcall ? P.kv.num_blocks : 0, live = kvcall ? P.kv.live_blocks : 0;
     for (const Launch &L : c.host_reads) {
-      if (!await) {
-        one(L);
-        continue;
-      }
       Launch piece = L;
       piece.bytes = 0;
       uint64_t end = 0;
@@ -578,22 +620,32 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
         end = std::max(end, extent(f, true, nb, live));  // source side: the inflow buffer
         if (piece.bytes >= kPipeBytes || d + 1 == L.d1) {
           piece.d1 = d + 1;
-          (*await)(end);
-          one(piece);
+          pieces.push_back({end, nullptr, piece});
           piece.d0 = d + 1;
           piece.bytes = 0;
+          end = 0;
         }
       }
     }
-    cs.hr1 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.hr1, s));
+    std::stable_sort(pieces.begin(), pieces.end(), [](const Piece &x, const Piece &y) { return x.end < y.end; });
+    for (const Piece &x : pieces) {
+      (*await)(x.end);
+      if (x.direct)
+        issue_direct(*x.direct);
+      else
+        host_read(x.L, s);
+    }
+    if (!c.host_reads.empty()) end_host_reads(s);
   };
   cs.hr1 = nullptr;
   // out of place: at once, on the side stream, beside the repack (the two
   // write disjoint bytes of the new arena)
   if (early_reads) {
     HIPCHK(hipStreamWaitEvent(E.side, prepared, 0));
-    issue_host_reads(E.side);
+    if (!await) {
+      for (const Launch &L : c.host_reads) host_read(L, E.side);
+      end_host_reads(E.side);
+    }
   }
 
   // ---- outbound (in place): read before overwrite ---------------------------------
@@ -686,7 +738,12 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // in place: the copy kernel reads every gated or strided inflow piece from
   // the pinned host buffer into its final place, after the last level (and,
   // for the weights, after every outbound read)
-  if (P.inplace && !c.host_reads.empty()) issue_host_reads(late_comp);
+  if (await) {
+    issue_awaited(P.inplace ? late_comp : E.side);
+  } else if (P.inplace && !c.host_reads.empty()) {
+    for (const Launch &L : c.host_reads) host_read(L, late_comp);
+    end_host_reads(late_comp);
+  }
 
   // KV outbound gathered into staging at level 0: copy it out after that level
   if (do_out && kvcall) {
@@ -879,8 +936,8 @@ void exec_warmup(void *compute_, void *copy_, int events) {
     E.ev_sync();
     E.ev_time();
   }
-  // two error words first: a call takes its 256-byte word before its
-  // descriptors, and the pool hands out the first buffer that is big enough
+  // error words and descriptor buffers for two calls (the pool hands out
+  // the smallest buffer that is big enough)
   std::vector<std::pair<void *, size_t>> bufs;
   for (size_t bytes : {size_t(256), size_t(256), size_t(1) << 20, size_t(1) << 20}) {
     size_t cap = 0;

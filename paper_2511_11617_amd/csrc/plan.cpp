@@ -98,6 +98,41 @@ void partition(int64_t H, int M, int rule, std::vector<Rng> &out) {
 namespace {
 
 // ---- problem intake ------------------------------------------------------------
+// The n ranges of one side (old or new) of space s from a rule other than GQA.
+void ranges_by_rule(int s, const char *side, int rule, int64_t H, int n, const atp_range *given,
+                    const int64_t *widths, std::vector<Rng> &out) {
+  const std::string where = "space " + std::to_string(s) + ": " + side;
+  if (rule == ATP_RULE_EXPLICIT) {
+    if (!given) fail(ATP_EINVAL, where + " ranges missing");
+    out.resize(n);
+    for (int j = 0; j < n; ++j) out[j] = {given[j].begin, given[j].end};
+  } else if (rule == ATP_RULE_FLOOR || rule == ATP_RULE_CEIL_FIRST) {
+    partition(H, n, rule, out);
+  } else if (rule == ATP_RULE_WIDTHS) {
+    if (!widths) fail(ATP_EINVAL, where + " widths missing");
+    out.resize(n);
+    int64_t at = 0;
+    for (int j = 0; j < n; ++j) {
+      if (widths[j] < 0 || widths[j] > H - at) fail(ATP_EINVAL, where + " widths must add up to total_units");
+      out[j] = {at, at + widths[j]};
+      at += widths[j];
+    }
+    if (at != H) fail(ATP_EINVAL, where + " widths must add up to total_units");
+  } else {
+    fail(ATP_EINVAL, where + " unknown rule");
+  }
+}
+
+// Every range inside [0, H) and together covering it.
+void check_cover(int s, const char *side, int64_t H, const std::vector<Rng> &r) {
+  const std::string where = "space " + std::to_string(s) + ": " + side;
+  for (size_t j = 0; j < r.size(); ++j)
+    if (r[j].b < 0 || r[j].e < r[j].b || r[j].e > H)
+      fail(ATP_EINVAL, where + " range " + std::to_string(j) + " out of bounds");
+  Set u = union_of(r);
+  if (u.size() != 1 || u[0].b != 0 || u[0].e != H) fail(ATP_EINVAL, where + " ranges do not cover [0, H)");
+}
+
 void resolve_spaces(Plan &P) {
   const atp_problem &p = P.prob;
   if (p.n_spaces <= 0 || !p.spaces) fail(ATP_EINVAL, "no partition spaces");
@@ -109,64 +144,47 @@ void resolve_spaces(Plan &P) {
     SpacePlan &sp = P.sp[s];
     if (in.old_tp != N || in.new_tp != M) fail(ATP_EINVAL, "every space must have the same old_tp and new_tp");
     if (in.total_units <= 0) fail(ATP_EINVAL, "space " + std::to_string(s) + ": total_units must be positive");
-    if (!in.old_ranges) fail(ATP_EINVAL, "space " + std::to_string(s) + ": old_ranges missing");
     sp.H = in.total_units;
     sp.N = N;
     sp.M = M;
-    sp.old_r.resize(N);
-    int64_t maxe = 0;
-    std::vector<Rng> all;
-    for (int i = 0; i < N; ++i) {
-      Rng r{in.old_ranges[i].begin, in.old_ranges[i].end};
-      if (r.b < 0 || r.e < r.b || r.e > sp.H)
-        fail(ATP_EINVAL, "space " + std::to_string(s) + ": old range of rank " + std::to_string(i) + " out of bounds");
-      sp.old_r[i] = r;
-      maxe = std::max(maxe, r.e);
-      all.push_back(r);
-    }
-    // Alg. 1: H is the largest end of any range, dead ranks included
-    if (maxe != sp.H) fail(ATP_EINVAL, "space " + std::to_string(s) + ": total_units must equal the largest old range end");
-    Set u = union_of(all);
-    if (u.size() != 1 || u[0].b != 0 || u[0].e != sp.H)
-      fail(ATP_EINVAL, "space " + std::to_string(s) + ": old ranges do not cover [0, H)");
   }
-  // new ranges: explicit and rule-based first, GQA-derived after
-  for (int pass = 0; pass < 2; ++pass) {
-    for (int s = 0; s < p.n_spaces; ++s) {
-      const atp_space &in = p.spaces[s];
-      SpacePlan &sp = P.sp[s];
-      bool gqa = in.new_rule == ATP_RULE_GQA;
-      if ((pass == 0) == gqa) continue;
-      if (in.new_rule == ATP_RULE_EXPLICIT) {
-        if (!in.new_ranges) fail(ATP_EINVAL, "space " + std::to_string(s) + ": new_ranges missing");
-        sp.new_r.resize(M);
-        for (int j = 0; j < M; ++j) sp.new_r[j] = {in.new_ranges[j].begin, in.new_ranges[j].end};
-      } else if (in.new_rule == ATP_RULE_FLOOR || in.new_rule == ATP_RULE_CEIL_FIRST) {
-        partition(sp.H, M, in.new_rule, sp.new_r);
-      } else if (gqa) {
-        int q = in.gqa_space;
-        if (q < 0 || q >= p.n_spaces || q == s || p.spaces[q].new_rule == ATP_RULE_GQA)
-          fail(ATP_EINVAL, "space " + std::to_string(s) + ": bad gqa_space");
-        if (in.gqa_group <= 0) fail(ATP_EINVAL, "space " + std::to_string(s) + ": gqa_group must be positive");
-        int64_t g = in.gqa_group;
-        sp.new_r.resize(M);
-        for (int j = 0; j < M; ++j) {
-          Rng qr = P.sp[q].new_r[j];
-          sp.new_r[j] = {qr.b / g, std::min<int64_t>(sp.H, (qr.e + g - 1) / g)};
+  // old ranges (rank order) and new ranges (target order): rule-based first,
+  // then those that follow a query-head space (GQA)
+  for (int side = 0; side < 2; ++side) {
+    const bool old_side = side == 0;
+    const char *name = old_side ? "old" : "new";
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int s = 0; s < p.n_spaces; ++s) {
+        const atp_space &in = p.spaces[s];
+        SpacePlan &sp = P.sp[s];
+        const int rule = old_side ? in.old_rule : in.new_rule;
+        const bool gqa = rule == ATP_RULE_GQA;
+        if ((pass == 0) == gqa) continue;
+        std::vector<Rng> &out = old_side ? sp.old_r : sp.new_r;
+        const int n = old_side ? N : M;
+        if (!gqa) {
+          ranges_by_rule(s, name, rule, sp.H, n, old_side ? in.old_ranges : in.new_ranges,
+                         old_side ? in.old_widths : in.new_widths, out);
+        } else {
+          int q = in.gqa_space;
+          if (q < 0 || q >= p.n_spaces || q == s ||
+              (old_side ? p.spaces[q].old_rule : p.spaces[q].new_rule) == ATP_RULE_GQA)
+            fail(ATP_EINVAL, "space " + std::to_string(s) + ": bad gqa_space");
+          if (in.gqa_group <= 0) fail(ATP_EINVAL, "space " + std::to_string(s) + ": gqa_group must be positive");
+          const int64_t g = in.gqa_group;
+          const std::vector<Rng> &qr = old_side ? P.sp[q].old_r : P.sp[q].new_r;
+          out.resize(n);
+          for (int j = 0; j < n; ++j) out[j] = {qr[j].b / g, std::min<int64_t>(sp.H, (qr[j].e + g - 1) / g)};
         }
-      } else {
-        fail(ATP_EINVAL, "space " + std::to_string(s) + ": unknown new_rule");
+        check_cover(s, name, sp.H, out);
+        if (old_side) {
+          // Alg. 1: H is the largest end of any range, dead ranks included
+          int64_t maxe = 0;
+          for (const Rng &r : out) maxe = std::max(maxe, r.e);
+          if (maxe != sp.H)
+            fail(ATP_EINVAL, "space " + std::to_string(s) + ": total_units must equal the largest old range end");
+        }
       }
-      std::vector<Rng> all;
-      for (int j = 0; j < M; ++j) {
-        Rng r = sp.new_r[j];
-        if (r.b < 0 || r.e < r.b || r.e > sp.H)
-          fail(ATP_EINVAL, "space " + std::to_string(s) + ": new range " + std::to_string(j) + " out of bounds");
-        all.push_back(r);
-      }
-      Set u = union_of(all);
-      if (u.size() != 1 || u[0].b != 0 || u[0].e != sp.H)
-        fail(ATP_EINVAL, "space " + std::to_string(s) + ": new ranges do not cover [0, H)");
     }
   }
 }

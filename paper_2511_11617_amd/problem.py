@@ -7,10 +7,12 @@ experts (MoE).  Tensors per layer, in arena order: wq, wk, wv (rows), wo
 (columns), then w_gate, w_up (rows), w_down (columns), or the expert
 tensors e_gate, e_up, e_down (rows of [experts * rows_per_expert, cols]).
 
-Old ranges default to an even split of each space, KV heads following the
-query heads (GQA); successive switches pass the previous new ranges as
-`old_ranges`.  New ranges are explicit widths when given, else
-ceil-first widths, KV heads GQA-derived unless widths are given.
+Only shapes, widths and rules are passed; the library derives every
+range.  Old ranges default to the even split of each space (the
+ceil-first rule), KV heads following the query heads (GQA); successive
+switches pass the previous new ranges as `old_ranges`.  New ranges are the
+stated widths when given, else the ceil-first rule (the floor rule of Alg. 1
+on request), KV heads GQA-derived unless widths are given.
 """
 from __future__ import annotations
 
@@ -26,10 +28,6 @@ _TENSORS_DENSE = [("wq", atp.ROWS, SPACE_Q), ("wk", atp.ROWS, SPACE_KV), ("wv", 
 _TENSORS_MOE = [("wq", atp.ROWS, SPACE_Q), ("wk", atp.ROWS, SPACE_KV), ("wv", atp.ROWS, SPACE_KV),
                 ("wo", atp.COLS, SPACE_Q), ("e_gate", atp.ROWS, SPACE_FFN),
                 ("e_up", atp.ROWS, SPACE_FFN), ("e_down", atp.ROWS, SPACE_FFN)]
-
-
-def _gqa(ranges, g):
-    return [(a // g, -(-b // g)) for a, b in ranges]
 
 
 def tensor_list(shape: dict):
@@ -68,16 +66,25 @@ def space_totals(shape: dict):
 class Built:
     """A Problem plus the arrays it points into."""
 
-    def __init__(self, problem, keep, tensors, n_live, pool, old_ranges):
+    def __init__(self, problem, keep, tensors, n_live, pool, n_spaces):
         self.problem = problem
         self.keep = keep
         self.tensors = tensors
         self.n_live = n_live
         self.pool = pool
-        self.old_ranges = old_ranges  # [space][old rank] -> (begin, end)
+        self.n_spaces = n_spaces
+        self._old = None
 
     def plan(self) -> atp.Plan:
         return atp.Plan(self.problem, keep=self.keep)
+
+    @property
+    def old_ranges(self):
+        """[space][old rank] -> (begin, end), as the library resolved them."""
+        if self._old is None:
+            p = self.plan()
+            self._old = [p.old_ranges(s) for s in range(self.n_spaces)]
+        return self._old
 
 
 def build(shape: dict, n_live: int | None = None, pool: int | None = None, flags: int = 0,
@@ -88,37 +95,38 @@ def build(shape: dict, n_live: int | None = None, pool: int | None = None, flags
     keep = []
     old_given = shape.get("old_ranges") or {}
     names = ["q", "kv", "exp" if shape.get("experts") else "ffn"]
-    old = {}
-    old["q"] = old_given.get("q") or atp.partition(totals[0], N, atp.RULE_CEIL_FIRST)
-    old["kv"] = old_given.get("kv") or _gqa(old["q"], g)
-    old[names[2]] = old_given.get(names[2]) or atp.partition(totals[2], N, atp.RULE_CEIL_FIRST)
     new_widths = {"q": shape.get("new_q_widths"), "kv": shape.get("new_kv_widths"),
                   "ffn": shape.get("new_ffn_widths"), "exp": shape.get("new_expert_widths")}
     new_given = shape.get("new_ranges") or {}
     spaces = (atp.Space * 3)()
+
+    def ranges(rs):
+        arr = (atp.Range * len(rs))(*[atp.Range(a, b) for a, b in rs])
+        keep.append(arr)
+        return C.cast(arr, C.POINTER(atp.Range))
+
     for s, name in enumerate(names):
         sp = spaces[s]
         sp.total_units = totals[s]
         sp.old_tp = N
         sp.new_tp = M
-        o = (atp.Range * N)(*[atp.Range(a, b) for a, b in old[name]])
-        keep.append(o)
-        sp.old_ranges = C.cast(o, C.POINTER(atp.Range))
-        rng = new_given.get(name)
-        if rng is None and new_widths[name] is not None:
-            at, rng = 0, []
-            for w in new_widths[name]:
-                rng.append((at, at + w))
-                at += w
-        if rng is not None:
-            n = (atp.Range * M)(*[atp.Range(a, b) for a, b in rng])
-            keep.append(n)
+        sp.gqa_space = SPACE_Q
+        sp.gqa_group = g
+        if old_given.get(name) is not None:
+            sp.old_rule = atp.RULE_EXPLICIT
+            sp.old_ranges = ranges(old_given[name])
+        else:
+            sp.old_rule = atp.RULE_GQA if name == "kv" else atp.RULE_CEIL_FIRST
+        if new_given.get(name) is not None:
             sp.new_rule = atp.RULE_EXPLICIT
-            sp.new_ranges = C.cast(n, C.POINTER(atp.Range))
+            sp.new_ranges = ranges(new_given[name])
+        elif new_widths[name] is not None:
+            w = (C.c_int64 * M)(*new_widths[name])
+            keep.append(w)
+            sp.new_rule = atp.RULE_WIDTHS
+            sp.new_widths = C.cast(w, C.POINTER(C.c_int64))
         elif name == "kv" and shape.get("kv_rule", "gqa") == "gqa":
             sp.new_rule = atp.RULE_GQA
-            sp.gqa_space = SPACE_Q
-            sp.gqa_group = g
         else:
             sp.new_rule = atp.RULE_FLOOR if shape.get("new_rule") == "floor" else atp.RULE_CEIL_FIRST
     tl = tensor_list(shape)
@@ -153,4 +161,4 @@ def build(shape: dict, n_live: int | None = None, pool: int | None = None, flags
                     pool, n_live)
         keep.append(kv)
         pb.kv = C.pointer(kv)
-    return Built(pb, keep, tl, n_live, pool, [old[n] for n in names])
+    return Built(pb, keep, tl, n_live, pool, len(names))

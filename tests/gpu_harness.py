@@ -59,14 +59,15 @@ def say(msg):
 
 
 def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
-             ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False):
+             ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False,
+             between=None):
     return prepare_case(c, flags, staging_cap, assign, check_outbound, name, variant, ckpt_dir, evict, pipelined,
-                        sparse_ckpt, kv_first, one_stream)()()
+                        sparse_ckpt, kv_first, one_stream, between=between)()()
 
 
 def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
                ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False,
-               streams=None):
+               streams=None, between=None):
     """Reshard one workload on the GPU and compare with the oracle.  With
     `ckpt_dir`, the weight inflow is read from a safetensors checkpoint
     written there by the library's range-read loader instead of being copied
@@ -76,7 +77,9 @@ def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=Tru
     packed inflow put back at its tensor coordinates), holes elsewhere.
     `kv_first` issues the KV call before the weights call (out of place
     only: in place that order is refused).  `one_stream` passes the same
-    stream as compute and copy stream.
+    stream as compute and copy stream.  `between(bufs, compute)` runs
+    between the two calls (bufs: dict of the device buffers), e.g. to queue
+    caller work on the compute stream that the second call must follow.
 
     prepare_case() builds the plan and the device and host buffers and
     returns issue(), which enqueues the reshard and returns finish(), which
@@ -197,13 +200,13 @@ def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=Tru
                         compute.cuda_stream, copy.cuda_stream)
 
     def issue():
+        first, second = (kv_call, weights_call) if kv_first else (weights_call, kv_call)
         if kv_first:
             assert not inplace, "in place the weights call comes first"
-            kv_call()
-            weights_call()
-        else:
-            weights_call()
-            kv_call()
+        first()
+        if between is not None:
+            between(dict(aw=aw, nw=nw, ak=ak, nk=nk, stage_w=stage_w, stage_k=stage_k), compute)
+        second()
         return finish
 
     def finish():

@@ -78,6 +78,49 @@ def test_bad_gqa_reference_is_einval():
     assert e.value.code == atp.EINVAL
 
 
+def test_old_and_new_ranges_from_rules():
+    """Old ranges from rules (even split, GQA from the query heads) and new
+    ranges from widths, all resolved by the library."""
+    c = configs.get(2)  # 40 q / 8 KV heads, TP 4 -> 3, q widths 14/13/13, KV widths 3/3/2
+    b = problem.build(c)
+    sp = b.problem.spaces
+    assert (sp[0].old_rule, sp[1].old_rule, sp[2].old_rule) == (atp.RULE_CEIL_FIRST, atp.RULE_GQA,
+                                                                 atp.RULE_CEIL_FIRST)
+    assert (sp[0].new_rule, sp[1].new_rule, sp[2].new_rule) == (atp.RULE_WIDTHS, atp.RULE_WIDTHS,
+                                                                 atp.RULE_CEIL_FIRST)
+    p = b.plan()
+    assert p.old_ranges(0) == [(0, 10), (10, 20), (20, 30), (30, 40)]
+    assert p.old_ranges(1) == [(0, 2), (2, 4), (4, 6), (6, 8)]
+    assert p.old_ranges(2) == [(0, 272), (272, 544), (544, 816), (816, 1088)]
+    assert p.ranges(0) == [(0, 14), (14, 27), (27, 40)]
+    assert p.ranges(1) == [(0, 3), (3, 6), (6, 8)]
+    assert p.ranges(2) == [(0, 363), (363, 726), (726, 1088)]
+    # the tiny workload: 4 q heads over 2 KV heads, GQA old and new
+    p1 = problem.build(configs.get(1)).plan()
+    assert p1.old_ranges(1) == [(0, 1), (0, 1), (1, 2), (1, 2)]
+    assert p1.ranges(1) == [(0, 1), (1, 2), (1, 2)]
+
+
+def test_bad_widths_and_old_gqa_reference_are_einval():
+    b = problem.build(configs.get(2))
+    w = b.problem.spaces[0].new_widths
+    w[2] = 12  # 14 + 13 + 12 != 40
+    with pytest.raises(atp.AtpError) as e:
+        b.plan()
+    assert e.value.code == atp.EINVAL and "widths" in str(e.value)
+    b = problem.build(configs.get(2))
+    b.problem.spaces[0].old_rule = atp.RULE_GQA  # the query-head space cannot follow itself
+    b.problem.spaces[0].gqa_space = 0
+    with pytest.raises(atp.AtpError) as e:
+        b.plan()
+    assert e.value.code == atp.EINVAL
+    b = problem.build(configs.get(2))
+    b.problem.spaces[2].old_rule = 9
+    with pytest.raises(atp.AtpError) as e:
+        b.plan()
+    assert e.value.code == atp.EINVAL and "unknown rule" in str(e.value)
+
+
 def test_in_place_staging_cap_too_small_is_ecapacity():
     c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=256)
     st = _plan(c, flags=atp.INPLACE, staging_cap=1 << 30).stats()
@@ -114,3 +157,29 @@ def test_warmup_without_a_gpu_and_with_a_bad_count():
     with pytest.raises(atp.AtpError) as e:
         atp.warmup(0, 0)
     assert e.value.code == atp.EHIP
+
+
+def test_staging_overlapping_an_arena_is_einval_before_any_gpu_call():
+    """Argument checks run before the first HIP call (fake addresses, no
+    GPU): staging may not overlap the arena it repacks."""
+    for flags in (0, atp.INPLACE):
+        p = _plan(configs.get(1), flags=flags)
+        st = p.stats()
+        A, N = 1 << 32, 1 << 34  # fake, 256-byte aligned device addresses
+        size = max(st.old_arena_bytes, st.new_arena_bytes)
+        new = None if flags else N
+        inside = A + 4096  # inside the old arena
+        with pytest.raises(atp.AtpError) as e:
+            p.reshard_weights(A, size, new, st.new_arena_bytes if new else 0, 1 << 36, st.inflow_w,
+                              1 << 37, st.outbound_w, inside, st.staging_w, 0, 0)
+        assert e.value.code == atp.EINVAL and "staging overlaps" in str(e.value)
+        if not flags:  # inside the new arena
+            with pytest.raises(atp.AtpError) as e:
+                p.reshard_weights(A, size, N, st.new_arena_bytes, 1 << 36, st.inflow_w, 1 << 37, st.outbound_w,
+                                  N + 256, st.staging_w, 0, 0)
+            assert e.value.code == atp.EINVAL and "staging overlaps" in str(e.value)
+        with pytest.raises(atp.AtpError) as e:  # the KV call too
+            p.reshard_kv(A, st.old_kv_bytes if flags == 0 else max(st.old_kv_bytes, st.new_kv_bytes),
+                         new, st.new_kv_bytes if new else 0, 1 << 38, 8, 8, 1 << 36, st.inflow_kv,
+                         1 << 37, st.outbound_kv, A, st.staging_kv, 0, 0)
+        assert e.value.code == atp.EINVAL and "staging overlaps" in str(e.value)

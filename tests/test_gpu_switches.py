@@ -223,3 +223,69 @@ def test_failed_pin_leaves_no_hip_error_behind():
     x = torch.full((1 << 20,), 7, dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     assert int(x[-1]) == 7
+
+
+def _direct_landing_cfg():
+    """2 layers, hidden 8192, TP 2 -> 1: the one target takes every tensor
+    whole, and the dead rank's half of W_gate / W_up (2048 rows x 8192, 32 MiB
+    each) lands by DMA straight into place."""
+    from synth.content import KIND_TAG16
+    return configs.get(1, layers=2, hidden=8192, n_q=16, n_kv=4, head_dim=128, ffn=4096, ffn_unit=16,
+                       old_tp=2, new_tp=1, failed=[1], self_old=0, new_q_widths=None, new_ffn_widths=None,
+                       n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+
+
+def test_caller_work_between_the_calls_comes_first():
+    """Each call starts after what the caller queued on the compute stream
+    before it, also when the other call of the plan is pending: the caller
+    fills the weights' new arena between the KV call and the weights call,
+    and the weights call's DMA landings still land over the fill."""
+    c = _direct_landing_cfg()
+
+    def fill(bufs, compute):
+        with torch.cuda.stream(compute):
+            bufs["nw"].fill_(0x77)
+
+    run_case(c, kv_first=True, between=fill, name="fill between calls")
+
+
+def test_pending_calls_sharing_staging_are_einval():
+    """The two calls of a plan may be pending together only on buffers of
+    their own: a KV call on the pending weights call's staging, or with its
+    new arena over the weights' new arena, is refused; the weights call
+    still completes."""
+    c = configs.get(1)
+    table, pool = pagetable.make_for(c)
+    pb = model.build(c)
+    content = Content(0, c["w_kind"], c["kv_kind"])
+    b = problem.build(c, n_live=len(repack.live_blocks(table)), pool=pool)
+    plan = b.plan()
+    st = plan.stats()
+    dev = torch.device("cuda")
+    aw = torch.from_numpy(repack.weight_arena(pb, content, "old")).to(dev)
+    nw = torch.empty(st.new_arena_bytes, dtype=torch.uint8, device=dev)
+    sw = torch.empty(max(st.staging_w, st.staging_kv), dtype=torch.uint8, device=dev)
+    ak = torch.from_numpy(repack.kv_arena(pb, content, table, pool, "old")).to(dev)
+    nk = torch.empty(st.new_kv_bytes, dtype=torch.uint8, device=dev)
+    sk = torch.empty(st.staging_kv, dtype=torch.uint8, device=dev)
+    hw = _pinned(repack.packed_weight_inflow(pb, content))
+    hk = _pinned(repack.packed_kv_inflow(pb, content, table, pool))
+    td = torch.from_numpy(table).to(dev)
+    s0, s1 = torch.cuda.current_stream(), torch.cuda.Stream()
+    plan.reshard_weights(aw.data_ptr(), aw.numel(), nw.data_ptr(), nw.numel(), hw.data_ptr(), st.inflow_w, None, 0,
+                         sw.data_ptr(), sw.numel(), s0.cuda_stream, s1.cuda_stream)
+
+    def kv(new, staging):
+        plan.reshard_kv(ak.data_ptr(), ak.numel(), new.data_ptr(), st.new_kv_bytes, td.data_ptr(), table.shape[0],
+                        table.shape[1], hk.data_ptr(), st.inflow_kv, None, 0, staging.data_ptr(),
+                        st.staging_kv, s0.cuda_stream, s1.cuda_stream)
+
+    for new, staging in ((nk, sw), (nw, sk)):
+        with pytest.raises(atp.AtpError) as e:
+            kv(new, staging)
+        assert e.value.code == atp.EINVAL and "overlaps" in str(e.value)
+    plan.sync()
+    torch.cuda.synchronize()
+    want = repack.weight_arena(pb, content, "new")
+    mask = repack.weight_live_mask(pb, "new")
+    np.testing.assert_array_equal(nw.cpu().numpy()[mask], want[mask])
