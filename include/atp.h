@@ -215,6 +215,30 @@ int atp_reshard_kv(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes,
                    void *staging, uint64_t staging_bytes,
                    atp_stream compute, atp_stream copy);
 
+/* atp_reshard_kv for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * reshard, with no staging argument.  Its descriptors, prefix sums, block
+ * lists and landing ring live in a file-scope device array of the library
+ * (atp_scratch_bytes() = 64 MiB, one copy per device, held until the process
+ * ends), and the call allocates nothing: its events, pinned descriptor
+ * buffers and side stream come from what atp_warmup(compute, copy, events)
+ * pooled on this device for these streams (run it first; running short is
+ * ATP_ESTATE, not an allocation).  A plan whose stats.staging_kv exceeds
+ * atp_scratch_bytes() is ATP_ECAPACITY (in place, plan with a staging_cap
+ * no larger).  Every call on a device shares that device's array: one
+ * such call may be pending per device at a time (another before its
+ * atp_sync is ATP_ESTATE); calls from several processes, or from threads
+ * that race past that check, on one device would corrupt each other.
+ * Nothing in the array needs to start at zero.  Other arguments, results
+ * and errors as for atp_reshard_kv. */
+int atp_reshard_kv_noalloc(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes,
+                           void *new_kv_arena, uint64_t new_kv_bytes,
+                           const int32_t *block_table, int32_t n_seq, int32_t max_blocks,
+                           const void *inflow_host, uint64_t inflow_bytes,
+                           void *outbound_host, uint64_t outbound_bytes,
+                           atp_stream compute, atp_stream copy);
+uint64_t atp_scratch_bytes(void);
+
 /* Timing of the last reshard (HIP events; host clock for wall_ms). */
 typedef struct {
   double plan_ms;      /* atp_plan host time                          */

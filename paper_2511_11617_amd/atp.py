@@ -38,6 +38,7 @@ EXPORTS = [
     "atp_kv_evict_lru", "atp_daemon_serve", "atp_state_connect", "atp_state_disconnect",
     "atp_state_alloc", "atp_state_open", "atp_state_release", "atp_state_free", "atp_state_put",
     "atp_state_get", "atp_state_list", "atp_state_shutdown", "atp_warmup", "atp_load_reshard_weights",
+    "atp_reshard_kv_noalloc", "atp_scratch_bytes",
 ]
 
 
@@ -154,6 +155,10 @@ def _load():
                                         P, C.c_uint64, P, P]
     lib.atp_reshard_kv.argtypes = [P, P, C.c_uint64, P, C.c_uint64, P, C.c_int32, C.c_int32, P,
                                    C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, P]
+    lib.atp_reshard_kv_noalloc.argtypes = [P, P, C.c_uint64, P, C.c_uint64, P, C.c_int32, C.c_int32, P,
+                                           C.c_uint64, P, C.c_uint64, P, P]
+    lib.atp_scratch_bytes.argtypes = []
+    lib.atp_scratch_bytes.restype = C.c_uint64
     lib.atp_sync.argtypes = [P, C.POINTER(Timing)]
     lib.atp_warmup.argtypes = [P, P, C.c_int32]
     lib.atp_plan_stats.argtypes = [P, C.POINTER(Stats)]
@@ -209,6 +214,11 @@ def _check(rc):
     if rc != OK:
         raise AtpError(rc, lib.atp_last_error().decode())
     return rc
+
+
+def scratch_bytes() -> int:
+    """Size of the no-allocation entry point's device scratch array."""
+    return int(lib.atp_scratch_bytes())
 
 
 def partition(total: int, parts: int, rule: int):
@@ -286,6 +296,12 @@ class Plan:
         _check(lib.atp_reshard_weights(self.h, arena, arena_bytes, new_arena, new_bytes, inflow,
                                        inflow_bytes, outbound, outbound_bytes, staging,
                                        staging_bytes, compute, copy))
+
+    def reshard_kv_noalloc(self, arena, arena_bytes, new_arena, new_bytes, table, n_seq, max_blocks,
+                           inflow, inflow_bytes, outbound, outbound_bytes, compute, copy):
+        _check(lib.atp_reshard_kv_noalloc(self.h, arena, arena_bytes, new_arena, new_bytes, table, n_seq,
+                                          max_blocks, inflow, inflow_bytes, outbound, outbound_bytes,
+                                          compute, copy))
 
     def reshard_kv(self, arena, arena_bytes, new_arena, new_bytes, table, n_seq, max_blocks,
                    inflow, inflow_bytes, outbound, outbound_bytes, staging, staging_bytes,

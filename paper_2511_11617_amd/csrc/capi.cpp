@@ -110,6 +110,23 @@ int atp_reshard_kv(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes, void *ne
   });
 }
 
+int atp_reshard_kv_noalloc(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes, void *new_kv_arena,
+                           uint64_t new_kv_bytes, const int32_t *block_table, int32_t n_seq, int32_t max_blocks,
+                           const void *inflow_host, uint64_t inflow_bytes, void *outbound_host,
+                           uint64_t outbound_bytes, atp_stream compute, atp_stream copy) {
+  return guard([&]() -> int {
+    if (!plan) return fail(ATP_EINVAL, "plan is NULL");
+    if (!plan->p->has_kv) return fail(ATP_EINVAL, "the problem has no KV cache");
+    if (n_seq <= 0 || max_blocks <= 0) return fail(ATP_EINVAL, "block table must have positive size");
+    atp::exec_call(*plan->p, true, kv_arena, kv_bytes, new_kv_arena, new_kv_bytes, inflow_host, inflow_bytes,
+                   outbound_host, outbound_bytes, block_table, int64_t(n_seq) * max_blocks, nullptr, 0,
+                   static_cast<hipStream_t>(compute), static_cast<hipStream_t>(copy), nullptr, true);
+    return ATP_OK;
+  });
+}
+
+uint64_t atp_scratch_bytes(void) { return atp::scratch_bytes(); }
+
 int atp_sync(atp_plan_t *plan, atp_timing *out) {
   return guard([&]() -> int {
     if (!plan) return fail(ATP_EINVAL, "plan is NULL");

@@ -52,6 +52,7 @@ struct Span {
 
 struct CallState {
   bool pending = false;
+  bool on_scratch = false;  // the pending call runs on the device's scratch array
   Span old_arena, new_arena, staging;  // what the pending call reads and writes
   Desc *desc_host = nullptr;  // pinned copy of the descriptors
   size_t desc_cap = 0;
@@ -84,6 +85,10 @@ std::map<int, DevicePool> g_pools;
 struct Exec {
   int device = -1;
   int grid_max = 2048;
+  // Set while a call of the no-allocation entry point is being issued:
+  // events, pinned buffers and the side stream then come from the pools
+  // atp_warmup filled, and running short is an error, not an allocation.
+  bool no_alloc = false;
   // In place: `side` runs the outbound gathers and their device-to-host
   // copies, the weight levels that wait for them and the weight inflow the
   // copy kernel reads after them.  Out of place it runs the copy kernel's
@@ -110,6 +115,7 @@ struct Exec {
           v.pop_back();
         }
       }
+      if (!e && no_alloc) throw Error(ATP_ESTATE, "no pooled event left: call atp_warmup with more events first");
       if (!e) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
       sync_pool.push_back(e);
     }
@@ -126,6 +132,7 @@ struct Exec {
           v.pop_back();
         }
       }
+      if (!e && no_alloc) throw Error(ATP_ESTATE, "no pooled event left: call atp_warmup with more events first");
       if (!e) HIPCHK(hipEventCreate(&e));
       time_pool.push_back(e);
     }
@@ -145,6 +152,9 @@ struct Exec {
         return p;
       }
     }
+    if (no_alloc)
+      throw Error(ATP_ESTATE, "no pooled pinned buffer of " + std::to_string(bytes) +
+                                  " bytes: call atp_warmup on this device first");
     void *p = nullptr;
     HIPCHK(hipHostMalloc(&p, bytes, hipHostMallocDefault));
     *cap = bytes;
@@ -269,6 +279,8 @@ void choose_side(Exec &E, hipStream_t compute, hipStream_t copy) {
     if (i < known.size()) {
       s = known[i];
     } else if (i < kSideStreams) {
+      if (E.no_alloc)
+        throw Error(ATP_ESTATE, "no side stream chosen for these streams: call atp_warmup(compute, copy) first");
       HIPCHK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));  // default priority
       std::lock_guard<std::mutex> g(g_pool_mu);
       g_pools[E.device].streams.push_back(s);
@@ -423,13 +435,56 @@ void launch_copy(Exec &E, const Launch &L, const Desc *dev_desc, const int64_t *
   HIPCHK(hipGetLastError());
 }
 
+// ---- the scratch array of the no-allocation entry point --------------------------
+// Callers that cannot allocate (code under HIP graph capture, tight serving
+// loops) reshard on this file-scope device array instead of a staging
+// buffer of their own.  Each device holds its own copy at its own address,
+// looked up once per device with that device current; host code uses that
+// address, never the array's name.
+constexpr uint64_t kScratchBytes = 64ull << 20;
+__device__ __align__(256) char scratch[kScratchBytes];
+std::map<int, void *> g_scratch;     // device -> address of its copy (under g_pool_mu)
+std::map<int, bool> g_scratch_busy;  // a call on it is pending (under g_pool_mu)
+
+void *scratch_of(int dev) {
+  std::lock_guard<std::mutex> g(g_pool_mu);
+  auto it = g_scratch.find(dev);
+  if (it != g_scratch.end()) return it->second;
+  void *p = nullptr;
+  HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+  if (!p || reinterpret_cast<uintptr_t>(p) % 256) throw Error(ATP_EHIP, "scratch array has no usable device address");
+  g_scratch[dev] = p;
+  return p;
+}
+
+void release_scratch(Exec &E, CallState &cs) {
+  if (!cs.on_scratch) return;
+  cs.on_scratch = false;
+  std::lock_guard<std::mutex> g(g_pool_mu);
+  g_scratch_busy[E.device] = false;
+}
+
 }  // namespace
+
+uint64_t scratch_bytes() { return kScratchBytes; }
 
 void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *new_arena, uint64_t new_bytes,
                const void *inflow_host, uint64_t inflow_bytes, void *outbound_host, uint64_t outbound_bytes,
                const int32_t *table, int64_t n_entries, void *staging, uint64_t staging_bytes, hipStream_t compute,
-               hipStream_t copy, const std::function<void(uint64_t)> *await) {
+               hipStream_t copy, const std::function<void(uint64_t)> *await, bool on_scratch) {
   CallPlan &c = kvcall ? P.k : P.w;
+  if (on_scratch) {
+    // the device's scratch array in place of a staging buffer
+    if (c.staging_need > kScratchBytes)
+      throw Error(ATP_ECAPACITY, std::string(kvcall ? "kv" : "weights") + ": the plan needs " +
+                                     std::to_string(c.staging_need) + " bytes of scratch; the no-allocation entry "
+                                     "point has " + std::to_string(kScratchBytes) +
+                                     " (plan with a staging cap no larger)");
+    int dev = -1;
+    HIPCHK(hipGetDevice(&dev));
+    staging = scratch_of(dev);
+    staging_bytes = kScratchBytes;
+  }
   // Every argument is checked before the first HIP call.  The executor's
   // state exists from the plan's first call on; before it nothing is pending.
   Exec *Ep = static_cast<Exec *>(P.exec);
@@ -496,6 +551,30 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
 
   Exec &E = exec_of(P);
   CallState &cs = kvcall ? E.k : E.w;
+  if (on_scratch) {
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    if (g_scratch_busy[E.device])
+      throw Error(ATP_ESTATE, "the device's scratch array is in use by a pending call: atp_sync it first");
+    g_scratch_busy[E.device] = true;
+  }
+  // from here on the call either is issued (pending) or gives back the
+  // scratch array, once nothing it enqueued can still be running
+  struct Undo {
+    Exec &E;
+    CallState &cs;
+    hipStream_t s0, s1;
+    bool armed = true, enqueued = false;
+    ~Undo() {
+      E.no_alloc = false;
+      if (!armed || !cs.on_scratch) return;
+      if (enqueued)
+        for (hipStream_t s : {s0, s1, E.side})
+          if (s && hipStreamSynchronize(s) != hipSuccess) (void)hipGetLastError();
+      release_scratch(E, cs);
+    }
+  } undo{E, cs, compute, copy};
+  cs.on_scratch = on_scratch;
+  E.no_alloc = on_scratch;
 
   int dev = -1;
   HIPCHK(hipGetDevice(&dev));
@@ -539,6 +618,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // `compute` when the call is made (with the other call of the plan
   // pending, that includes the other call's work on `compute`)
   cs.start = E.ev_sync();
+  undo.enqueued = true;
   HIPCHK(hipEventRecord(cs.start, compute));
   HIPCHK(hipStreamWaitEvent(copy, cs.start, 0));
 
@@ -805,6 +885,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     HIPCHK(hipEventRecord(cs.tail_side, E.side));
   }
   cs.pending = true;
+  undo.armed = false;
 }
 
 int exec_sync(Plan &P, atp_timing *out) {
@@ -836,6 +917,7 @@ int exec_sync(Plan &P, atp_timing *out) {
       }
     }
     cs.pending = false;
+    release_scratch(E, cs);
     if (*cs.err_host && rc == ATP_OK) {
       rc = ATP_EINVAL;
       msg = "block table invalid:";
@@ -906,10 +988,12 @@ void exec_free(Plan &P) {
   if (P.exec) {
     Exec *E = static_cast<Exec *>(P.exec);
     // drain anything still queued before the pinned buffers go away
-    for (CallState *c : {&E->w, &E->k})
+    for (CallState *c : {&E->w, &E->k}) {
       if (c->pending)
         for (hipEvent_t e : {c->tail_compute, c->tail_copy, c->tail_side})
           if (e) (void)hipEventSynchronize(e);
+      release_scratch(*E, *c);
+    }
     delete E;
     P.exec = nullptr;
   }
@@ -932,6 +1016,7 @@ void exec_warmup(void *compute_, void *copy_, int events) {
   HIPCHK(hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(&k_spin)));
   HIPCHK(hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(&k_nop)));
   choose_side(E, compute, copy);
+  (void)scratch_of(E.device);  // the no-allocation entry point's scratch array, on this device
   for (int i = 0; i < events; ++i) {
     E.ev_sync();
     E.ev_time();
