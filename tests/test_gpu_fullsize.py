@@ -7,6 +7,9 @@ the result is compared with the oracle's definition evaluated word by
 word: a random sample of every arena, the first and last bytes of every
 weight shard, all of layer 0's weights, and whole KV blocks.  The in-place
 workload also checks the outbound bytes read out before the overwrite.
+Then every byte of the new shard (and of the outbound buffer) is compared
+on the device with the content the seeded generator writes from the
+oracle's description of the new layout.
 """
 import numpy as np
 import pytest
@@ -14,7 +17,7 @@ import torch
 
 from oracle import model, repack
 from paper_2511_11617_amd import atp, problem
-from synth import configs, fill, pagetable
+from synth import configs, fill, gpu, pagetable
 from synth.pinned import Pageable, Pinned, host_buffers
 from synth.content import Content
 from tests.gpu_harness import say
@@ -57,8 +60,91 @@ def _pin_all(sizes, force_pageable=False):
     return bufs
 
 
-def run_full(n, inplace=None, pageable_kv_inflow=False):
-    c = configs.get(n, **({} if inplace is None else {"inplace": inplace}))
+def _every_byte(pb, content, table, pool, live, w_arena, k_arena, hout_w, w_out):
+    """Every byte of the new shard, compared on the device with the content
+    the seeded generator writes from the oracle's description of the new
+    layout (weights one layer at a time, KV one (layer, K|V) plane at a
+    time, free blocks and alignment padding excepted), and, in place, every
+    byte of the outbound buffer against the oracle's outbound segments."""
+    dev = torch.device("cuda")
+    n_offs, n_size = pb.layout("new")
+    starts = [i for i, t in enumerate(pb.tensors) if i == 0 or t.layer != pb.tensors[i - 1].layer]
+    bounds = [n_offs[i] for i in starts] + [n_size]
+    buf = torch.empty(max(b - a for a, b in zip(bounds, bounds[1:])), dtype=torch.uint8, device=dev)
+    checked = 0
+    for k, i0 in enumerate(starts):
+        i1 = starts[k + 1] if k + 1 < len(starts) else len(pb.tensors)
+        base = bounds[k]
+        shards = []
+        for i in range(i0, i1):
+            t = pb.tensors[i]
+            a, b = pb.new_range(t.space)
+            shards.append((t.tag, t.layer, t.kind == model.ROWS, t.rows, t.cols, t.unit, a, b, n_offs[i] - base))
+        fill.weights(buf, content, shards)
+        for i in range(i0, i1):
+            t = pb.tensors[i]
+            r, cc = t.shard_shape(pb.new_range(t.space))
+            nb = r * cc * pb.eb
+            o = n_offs[i]
+            if not torch.equal(w_arena[o:o + nb], buf[o - base:o - base + nb]):
+                bad = int((w_arena[o:o + nb] != buf[o - base:o - base + nb]).sum())
+                raise AssertionError(f"weights: tensor {t.name} layer {t.layer}: {bad} bytes differ")
+            checked += nb
+    del buf
+    # KV: plane by plane; only live blocks are defined
+    h0, h1 = pb.kv_heads("new")
+    block = pb.kv_block_bytes("new")
+    plane = pool * block
+    s_idx, b_idx = np.nonzero(table >= 0)
+    first = {}
+    for s_, b_ in zip(s_idx, b_idx):
+        first.setdefault(int(table[s_, b_]), (s_, b_))
+    ids = np.array(sorted(first), np.int64)
+    seq = torch.from_numpy(np.array([first[p][0] for p in ids], np.int32)).to(dev)
+    blk = torch.from_numpy(np.array([first[p][1] for p in ids], np.int32)).to(dev)
+    pos = torch.from_numpy(ids).to(dev)
+    live_d = torch.from_numpy(ids).to(dev)
+    assert np.array_equal(ids, live)
+    kbuf = torch.empty(plane, dtype=torch.uint8, device=dev)
+    lay = atp.KV_TOKEN_MAJOR if pb.kv_layout == "token" else atp.KV_HEAD_MAJOR
+    for l in range(pb.n_layers):
+        for which in (0, 1):
+            tag = 10 + which
+            kind, sigma = content.kind_sigma(tag)
+            kbuf.fill_(0)
+            gpu.fill_kv(kbuf, 0, seq, blk, pos, block, lay, h0, h1, pb.n_kv, pb.cfg["seq_tokens"],
+                        pb.block_tokens, pb.head_dim, content.key(tag, l), kind, sigma)
+            g = 2 * l + which
+            got = k_arena[g * plane:(g + 1) * plane].view(pool, block).index_select(0, live_d)
+            want = kbuf.view(pool, block).index_select(0, live_d)
+            if not torch.equal(got, want):
+                raise AssertionError(f"kv: layer {l} {'KV'[which]}: {int((got != want).sum())} bytes differ")
+            checked += got.numel()
+    del kbuf
+    if hout_w is not None and w_out:
+        total = sum(sg[-1] for sg in w_out)
+        ob = torch.empty(total, dtype=torch.uint8, device=dev)
+        fill.weights(ob, content, [(pb.tensors[sg[0]].tag, sg[1], pb.tensors[sg[0]].kind == model.ROWS,
+                                    pb.tensors[sg[0]].rows, pb.tensors[sg[0]].cols, pb.tensors[sg[0]].unit,
+                                    sg[4], sg[5], sg[6]) for sg in w_out])
+        step = 1 << 30
+        for a in range(0, total, step):
+            b = min(total, a + step)
+            got = hout_w.tensor[a:b].to(dev)
+            if not torch.equal(got, ob[a:b]):
+                raise AssertionError(f"outbound: {int((got != ob[a:b]).sum())} bytes differ in [{a}, {b})")
+        checked += total
+        del ob
+    torch.cuda.synchronize()
+    say(f"[fullsize] every byte checked: {checked / 1e9:.2f} GB")
+    return checked
+
+
+def run_full(n, inplace=None, pageable_kv_inflow=False, cfg=None, corrupt=None):
+    """`cfg` replaces workload n's shape; `corrupt(w_arena, k_arena, hout_w)`
+    changes the result before the every-byte check (to show it is not
+    vacuous)."""
+    c = cfg if cfg is not None else configs.get(n, **({} if inplace is None else {"inplace": inplace}))
     pb = model.build(c)
     content = Content(c["seed"], c["w_kind"], c["kv_kind"])
     table, pool = pagetable.make_for(c)
@@ -156,8 +242,17 @@ def run_full(n, inplace=None, pageable_kv_inflow=False):
         ow = repack.expected_packed_weight_words(pb, content, w_out, oo)
         _check("outbound", hout_w.tensor.numpy().view(np.uint16)[oo // 2], ow, np.ones(oo.shape, bool))
     assert st.global_reload == st.reload_min
-    for h in (hin_w, hin_k, hout_w, hout_k):
-        h.close()
+    # every byte, on the device (the sampled words above anchor it to the oracle on the CPU)
+    del stage_w, stage_k
+    torch.cuda.empty_cache()
+    try:
+        if corrupt is not None:
+            corrupt(w_arena, k_arena, hout_w)
+            torch.cuda.synchronize()
+        _every_byte(pb, content, table, pool, live, w_arena, k_arena, hout_w if inplace else None, w_out)
+    finally:
+        for h in (hin_w, hin_k, hout_w, hout_k):
+            h.close()
     return t
 
 
@@ -177,3 +272,23 @@ def test_full_size_workload_2_in_place_kv_inflow_pageable():
     so it may sit in ordinary host memory (the fallback of hosts that
     cannot pin every buffer of the 80-layer workload)."""
     run_full(2, inplace=True, pageable_kv_inflow=True)
+
+
+@pytest.mark.parametrize("where", ["weights", "kv", "outbound"])
+def test_every_byte_check_catches_one_wrong_byte(where):
+    """The device-side every-byte comparison fails when one byte of the
+    result is changed after the reshard (2 layers of the 80-layer TP 8 -> 7
+    shape in place, 4 sequences)."""
+    c = configs.scaled(5, layers=2, n_seq=4, seq_tokens=1024)
+
+    def flip(w, k, hout):
+        if where == "weights":
+            w[12345] ^= 1
+        elif where == "kv":
+            k[k.numel() // 2 + 4096 + 17] ^= 0x80
+        else:
+            hout.tensor[777] ^= 4
+
+    run_full(5, cfg=c)  # unchanged: passes
+    with pytest.raises(AssertionError, match=where):
+        run_full(5, cfg=c, corrupt=flip)
