@@ -225,12 +225,11 @@ int atp_reshard_kv(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes,
  * pooled on this device for these streams (run it first; running short is
  * ATP_ESTATE, not an allocation).  A plan whose stats.staging_kv exceeds
  * atp_scratch_bytes() is ATP_ECAPACITY (in place, plan with a staging_cap
- * no larger).  Every call on a device shares that device's array: one
- * such call may be pending per device at a time (another before its
- * atp_sync is ATP_ESTATE); calls from several processes, or from threads
- * that race past that check, on one device would corrupt each other.
- * Nothing in the array needs to start at zero.  Other arguments, results
- * and errors as for atp_reshard_kv. */
+ * no larger).  Every such call of a process on one device shares that
+ * device's array (each process loads its own), so two of them pending at
+ * once would race on it: a second call before the first one's atp_sync is
+ * refused with ATP_ESTATE.  Nothing in the array needs to start at zero.
+ * Other arguments, results and errors as for atp_reshard_kv. */
 int atp_reshard_kv_noalloc(atp_plan_t *plan, void *kv_arena, uint64_t kv_bytes,
                            void *new_kv_arena, uint64_t new_kv_bytes,
                            const int32_t *block_table, int32_t n_seq, int32_t max_blocks,
