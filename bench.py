@@ -456,10 +456,12 @@ def dominant_launch(launches):
     (dk, dl, db), dms = max(per.items(), key=lambda kv: kv[0][2]) if per else ((0, 0, 0), [0.0])
     dom_ms = sum(dms) / len(dms)
     dom_gbps = 2 * db / (dom_ms * 1e-3) / 1e9 if dom_ms > 0 else 0.0
+    # the eight launches that move the most bytes, in call and level order
+    top = sorted(sorted(per.items(), key=lambda kv: -kv[0][2])[:8])
     kernels = [{"call": "weights" if k == 0 else "kv",
                 "level": l, "alg_bytes": 2 * b, "avg_ms": round(sum(v) / len(v), 4),
                 "GBps": round(2 * b / (sum(v) / len(v) * 1e-3) / 1e9, 1)}
-               for (k, l, b), v in sorted(per.items())][:8]
+               for (k, l, b), v in top]
     return dk, db, dom_ms, dom_gbps, kernels
 
 
