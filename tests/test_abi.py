@@ -183,3 +183,35 @@ def test_staging_overlapping_an_arena_is_einval_before_any_gpu_call():
                          new, st.new_kv_bytes if new else 0, 1 << 38, 8, 8, 1 << 36, st.inflow_kv,
                          1 << 37, st.outbound_kv, A, st.staging_kv, 0, 0)
         assert e.value.code == atp.EINVAL and "staging overlaps" in str(e.value)
+
+
+def test_old_widths_and_floor_rules_give_the_same_plan_as_explicit_ranges():
+    """Old ranges from widths or the floor rule plan exactly like the same
+    ranges given explicitly (tasks of every space, statistics)."""
+    c = configs.get(1, old_ranges={"q": [(0, 1), (1, 2), (2, 3), (3, 4)]})
+    ref = _plan(c)
+    for rule in (atp.RULE_WIDTHS, atp.RULE_FLOOR):
+        b = problem.build(c)
+        sp = b.problem.spaces[0]
+        sp.old_rule = rule
+        if rule == atp.RULE_WIDTHS:
+            w = (C.c_int64 * 4)(1, 1, 1, 1)
+            b.keep.append(w)
+            sp.old_widths = C.cast(w, C.POINTER(C.c_int64))
+        p = b.plan()
+        assert p.old_ranges(0) == [(0, 1), (1, 2), (2, 3), (3, 4)]
+        for s in range(3):
+            assert p.tasks(s) == ref.tasks(s)
+        sa, sb = p.stats(), ref.stats()
+        for f, _ in atp.Stats._fields_:
+            assert getattr(sa, f) == getattr(sb, f), f
+    # unequal old widths 2 / 1 / 1 / 0 query heads, the KV heads following them (GQA)
+    b = problem.build(configs.get(1))
+    sp = b.problem.spaces[0]
+    sp.old_rule = atp.RULE_WIDTHS
+    w = (C.c_int64 * 4)(2, 1, 1, 0)
+    b.keep.append(w)
+    sp.old_widths = C.cast(w, C.POINTER(C.c_int64))
+    p = b.plan()
+    assert p.old_ranges(0) == [(0, 2), (2, 3), (3, 4), (4, 4)]
+    assert p.old_ranges(1) == [(0, 1), (1, 2), (1, 2), (2, 2)]
