@@ -13,7 +13,7 @@ Paper passages followed:
   * Eq. 1, Sec. III-C: the minimum reload is the sum over targets of the
     target size minus the part of it that surviving sources cover.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
   * target widths are an input; rules "floor" (Alg. 1) and "ceil_first"
     (larger shards first, as the workloads state) generate them;
   * target j is hosted by the j-th alive old rank in ascending order

@@ -2,8 +2,8 @@
 
 TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
 
-Readings of the paper (Sec. III-B layout invariants, Sec. III-C/IV "unified
-one-dimensional space"; each is listed in the design doc):
+Readings of the paper (Sec. III-B layout invariants; Sec. III-C and IV plan
+over one linear byte space per rank):
   * planning is done per partition space in units that must not be cut: a
     query head, a KV head, a group of FFN columns, an expert;
   * weights are [out, in] row-major; column-parallel tensors (Wq, Wk, Wv,
