@@ -605,6 +605,46 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   int32_t *dev_err = reinterpret_cast<int32_t *>(b_st + c.off_meta);
   int32_t *dev_live = kvcall ? reinterpret_cast<int32_t *>(b_st + c.off_kvlive) : nullptr;
 
+  // Every event recorded on a stream costs it a few microseconds (about
+  // 4.5 us each on the MI355X, against 2 us between two bare launches), so
+  // the launches of a stream share their timing marks: a launch that comes
+  // right after a timed one starts at that launch's end mark, and the
+  // events other streams wait on are those same marks.  mark[s] is the end
+  // mark of the last command queued on s when that command was a timed
+  // launch; `other(s)` forgets it when anything else is queued there.
+  std::map<hipStream_t, hipEvent_t> mark;
+  auto other = [&](hipStream_t st) { mark.erase(st); };
+  auto record = [&](hipEvent_t e, hipStream_t st) {
+    HIPCHK(hipEventRecord(e, st));
+    other(st);
+  };
+  auto timed = [&](int kind, int level, uint64_t bytes, hipStream_t st, const auto &launch) {
+    CallState::LaunchRec r{kind, level, bytes, nullptr, E.ev_time()};
+    auto it = mark.find(st);
+    if (it != mark.end()) {
+      r.e0 = it->second;
+    } else {
+      r.e0 = E.ev_time();
+      HIPCHK(hipEventRecord(r.e0, st));
+    }
+    launch();
+    HIPCHK(hipEventRecord(r.e1, st));
+    mark[st] = r.e1;
+    cs.launches.push_back(r);
+    return r;
+  };
+  // an event that fires once everything queued on st so far is done: the
+  // last end mark there, or a fresh event (a fresh timing event is then the
+  // mark a following launch starts at)
+  auto mark_or_record = [&](hipStream_t st, bool timing) {
+    auto it = mark.find(st);
+    if (it != mark.end()) return it->second;
+    hipEvent_t e = timing ? E.ev_time() : E.ev_sync();
+    HIPCHK(hipEventRecord(e, st));
+    if (timing) mark[st] = e;
+    return e;
+  };
+
   // The side stream runs, in place, the weights call's outbound reads,
   // levels and host reads and the KV call's outbound copies; out of place,
   // the host reads of both calls, beside the repack on `compute`.  It is
@@ -657,26 +697,22 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // k_prepare is the only writer of the error word: it stores it once
   hipLaunchKernelGGL(k_prepare, dim3(1), dim3(1024), 0, compute, pa);
   HIPCHK(hipGetLastError());
+  other(compute);
   hipEvent_t prepared = nullptr;  // descriptors, prefix sums and live blocks in place
   if (use_side) {
     prepared = E.ev_sync();
-    HIPCHK(hipEventRecord(prepared, compute));
+    record(prepared, compute);
   }
 
   // the copy kernel reads inflow pieces from the pinned host buffer into
   // their final place (kind 4 launches)
   auto host_read = [&](const Launch &L, hipStream_t s) {
-    CallState::LaunchRec r{4, -1, L.bytes, E.ev_time(), E.ev_time()};
-    HIPCHK(hipEventRecord(r.e0, s));
-    launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s, kHostReadGrid);
-    HIPCHK(hipEventRecord(r.e1, s));
-    cs.launches.push_back(r);
+    timed(4, -1, L.bytes, s, [&] {
+      launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s, kHostReadGrid);
+    });
     cs.h2d_bytes += L.bytes;
   };
-  auto end_host_reads = [&](hipStream_t s) {
-    cs.hr1 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.hr1, s));
-  };
+  auto end_host_reads = [&](hipStream_t s) { cs.hr1 = mark_or_record(s, true); };
   // While the inflow buffer is still being filled (`await`), the direct
   // landings and the host reads (each launch cut at descriptor boundaries
   // into pieces of at least kPipeBytes) are issued in the order of the end
@@ -710,10 +746,12 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     std::stable_sort(pieces.begin(), pieces.end(), [](const Piece &x, const Piece &y) { return x.end < y.end; });
     for (const Piece &x : pieces) {
       (*await)(x.end);
-      if (x.direct)
+      if (x.direct) {
         issue_direct(*x.direct);
-      else
+      } else {
+        other(s);  // the launch starts once the host has waited: it gets a start mark of its own
         host_read(x.L, s);
+      }
     }
     if (!c.host_reads.empty()) end_host_reads(s);
   };
@@ -722,6 +760,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // write disjoint bytes of the new arena)
   if (early_reads) {
     HIPCHK(hipStreamWaitEvent(E.side, prepared, 0));
+    other(E.side);
     if (!await) {
       for (const Launch &L : c.host_reads) host_read(L, E.side);
       end_host_reads(E.side);
@@ -732,26 +771,21 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // The weights call's outbound reads are copy-kernel launches on the side
   // stream that write straight into the pinned outbound buffer, in the
   // plan's order (by the first level that overwrites them), each level right
-  // after the reads it needs; pos_ev[k] fires when the first k + 1 have
-  // finished (pos_ev.size() is the number of pieces issued).  That work and
-  // the weight inflow read after it stay off the caller's streams, so that
-  // they do not hold up the other call's work queued behind them.
-  std::vector<hipEvent_t> pos_ev;
+  // after the reads it needs (stream order on that one stream is the gate).
+  // That work and the weight inflow read after it stay off the caller's
+  // streams, so that they do not hold up the other call's work queued
+  // behind them.
+  size_t issued = 0;  // outbound pieces read out so far, in plan order
   const bool split = do_out && !kvcall;
   hipStream_t late_comp = compute;
   if (split) {
     late_comp = E.side;  // the outbound launches read the descriptors
     HIPCHK(hipStreamWaitEvent(late_comp, prepared, 0));
+    other(late_comp);
   }
   std::vector<size_t> pos_of(c.outbound.size(), 0);
   for (size_t p = 0; p < c.out_order.size(); ++p) pos_of[size_t(c.out_order[p])] = p;
   auto issue_outbound = [&](size_t upto) {  // read out the first `upto` pieces
-    size_t issued = pos_ev.size();
-    if (issued >= upto) return;
-    if (!cs.d2h0) {
-      cs.d2h0 = E.ev_time();
-      HIPCHK(hipEventRecord(cs.d2h0, late_comp));
-    }
     while (issued < upto) {
       // one launch per run of positions with the same alignment
       Launch L;
@@ -763,26 +797,18 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
         L.bytes += c.outbound[size_t(c.out_order[issued])].bytes;
       }
       L.d1 = c.out_d0 + int(issued);
-      CallState::LaunchRec r{3, -1, L.bytes, E.ev_time(), E.ev_time()};
-      HIPCHK(hipEventRecord(r.e0, late_comp));
-      launch_copy(E, L, dev_desc, dev_prefix, b_in, host_out, b_st, dev_live, late_comp, kOutboundGrid);
-      HIPCHK(hipEventRecord(r.e1, late_comp));
-      cs.launches.push_back(r);
+      const CallState::LaunchRec r = timed(3, -1, L.bytes, late_comp, [&] {
+        launch_copy(E, L, dev_desc, dev_prefix, b_in, host_out, b_st, dev_live, late_comp, kOutboundGrid);
+      });
+      if (!cs.d2h0) cs.d2h0 = r.e0;
+      cs.d2h1 = r.e1;
       cs.d2h_bytes += L.bytes;
     }
-    hipEvent_t done = E.ev_sync();
-    HIPCHK(hipEventRecord(done, late_comp));
-    pos_ev.resize(upto, done);
   };
   cs.d2h0 = cs.d2h1 = nullptr;
 
   // ---- repack levels ---------------------------------------------------------------
-  std::vector<hipEvent_t> level_end(std::max(c.n_levels, 1), nullptr);
-  auto begin_levels = [&]() {
-    if (cs.rep0) return;
-    cs.rep0 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.rep0, late_comp));
-  };
+  hipEvent_t level0_end = nullptr;  // the KV outbound gathered at level 0 is copied out after it
   cs.rep0 = nullptr;
   for (size_t i = 0; i < c.levels.size(); ++i) {
     const Launch &L = c.levels[i];
@@ -791,29 +817,16 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
       for (int o : L.wait_outbound) need = std::max(need, pos_of[size_t(o)] + 1);
       issue_outbound(need);
     }
-    begin_levels();
-    CallState::LaunchRec r{kvcall ? 1 : 0, L.level, L.bytes, E.ev_time(), E.ev_time()};
-    HIPCHK(hipEventRecord(r.e0, late_comp));
-    launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
-    HIPCHK(hipEventRecord(r.e1, late_comp));
-    cs.launches.push_back(r);
+    const CallState::LaunchRec r = timed(kvcall ? 1 : 0, L.level, L.bytes, late_comp, [&] {
+      launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
+    });
+    if (!cs.rep0) cs.rep0 = r.e0;
     cs.repack_bytes += 2 * L.bytes;
-    bool last_of_level = i + 1 == c.levels.size() || c.levels[i + 1].level != L.level;
-    if (last_of_level) {
-      level_end[L.level] = E.ev_sync();
-      HIPCHK(hipEventRecord(level_end[L.level], late_comp));
-    }
+    if (L.level == 0) level0_end = r.e1;
   }
-  if (split) {
-    issue_outbound(c.out_order.size());  // pieces no level waits for
-    if (cs.d2h0) {
-      cs.d2h1 = E.ev_time();
-      HIPCHK(hipEventRecord(cs.d2h1, late_comp));
-    }
-  }
-  begin_levels();
-  cs.rep1 = E.ev_time();
-  HIPCHK(hipEventRecord(cs.rep1, late_comp));  // also: prepare and every level are done
+  if (split) issue_outbound(c.out_order.size());  // pieces no level waits for
+  if (!cs.rep0) cs.rep0 = mark_or_record(late_comp, true);
+  cs.rep1 = mark_or_record(late_comp, true);  // also: prepare and every level are done
 
   // in place: the copy kernel reads every gated or strided inflow piece from
   // the pinned host buffer into its final place, after the last level (and,
@@ -827,16 +840,16 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
 
   // KV outbound gathered into staging at level 0: copy it out after that level
   if (do_out && kvcall) {
-    if (level_end[0]) HIPCHK(hipStreamWaitEvent(E.side, level_end[0], 0));
+    if (level0_end) HIPCHK(hipStreamWaitEvent(E.side, level0_end, 0));
     cs.d2h0 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.d2h0, E.side));
+    record(cs.d2h0, E.side);
     for (size_t o = 0; o < c.outbound.size(); ++o) {
       const HostCopy &h = c.outbound[o];
       HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_st + h.dev_off, h.bytes, hipMemcpyDeviceToHost, E.side));
       cs.d2h_bytes += h.bytes;
     }
     cs.d2h1 = E.ev_time();
-    HIPCHK(hipEventRecord(cs.d2h1, E.side));
+    record(cs.d2h1, E.side);
   }
 
   // ---- inflow ------------------------------------------------------------------------
@@ -857,16 +870,13 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     hipEvent_t landed = E.ev_sync();
     HIPCHK(hipEventRecord(landed, copy));
     HIPCHK(hipStreamWaitEvent(late_comp, landed, 0));
+    other(late_comp);
     for (const Launch &L : ch.scatters) {
-      CallState::LaunchRec r{2, -1, L.bytes, E.ev_time(), E.ev_time()};
-      HIPCHK(hipEventRecord(r.e0, late_comp));
-      launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
-      HIPCHK(hipEventRecord(r.e1, late_comp));
-      cs.launches.push_back(r);
+      timed(2, -1, L.bytes, late_comp,
+            [&] { launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp); });
       cs.scatter_bytes += L.bytes;
     }
-    slot_free[i] = E.ev_sync();
-    HIPCHK(hipEventRecord(slot_free[i], late_comp));
+    slot_free[i] = mark_or_record(late_comp, false);  // the chunk's last scatter is done
   }
   cs.h2d1 = E.ev_time();  // the inflow ends with the later of this and hr1
   HIPCHK(hipEventRecord(cs.h2d1, copy));
