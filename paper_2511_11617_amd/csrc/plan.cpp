@@ -638,6 +638,14 @@ bool is_identity(const Fam &f) {
 }
 
 constexpr uint64_t kSplitLine = 64 * 1024;
+constexpr uint64_t kRingSlots = 4, kRingSlotMax = 256ull << 20;  // landing ring of the in-place KV inflow
+// Tail staging (schedule): the cost of one more level (its launch and the gap
+// before the next, measured at 15-20 us for small levels on the MI355X), the
+// copy rate of the extra staging traffic (bytes of traffic per second), and
+// the most bytes routed that way.
+constexpr double kLevelCost = 15e-6;
+constexpr double kTailRate = 6e12;
+constexpr uint64_t kTailMax = 256ull << 20;
 constexpr uint64_t kDirectMin = 32ull << 20;  // smallest inflow gap landed directly
 constexpr size_t kMaxPieces = 1u << 20;
 
@@ -785,6 +793,9 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
   std::vector<Node> nodes;
   std::vector<Fam> to_stage;
   uint64_t stage_bytes = 0;
+  auto moved_of = [&](const Node &x) {
+    return uint64_t(std::min<int64_t>(x.fam.o_end - x.fam.o_begin, live_hint)) * x.fam.rows * x.fam.run;
+  };
 
   if (!P.inplace) {
     for (Fam &f : retained) {
@@ -799,7 +810,7 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
       size_t budget = 4096;
       split_family(f, nodes, to_stage, budget);
     }
-    for (Node &n : nodes) c.moved += uint64_t(std::min<int64_t>(n.fam.o_end - n.fam.o_begin, live_hint)) * n.fam.rows * n.fam.run;
+    for (Node &n : nodes) c.moved += moved_of(n);
     for (Fam &f : to_stage) {
       Node n;
       n.kind = Node::STAGED;
@@ -817,6 +828,25 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
         nodes.push_back(n);
       }
     }
+  }
+
+  // Staging room for the tail of the level chain (below): what the cap
+  // leaves after the pieces already staged, the KV outbound gathered there,
+  // the landing ring at its full size and the descriptor and block-list
+  // area, at most kTailMax.
+  uint64_t tail_room = 0;
+  if (P.inplace) {
+    uint64_t used = 0;
+    for (const Node &x : nodes)
+      if (x.kind != Node::NORMAL) used += align_up(x.kind == Node::GATHER ? x.fam.bytes() : moved_of(x), 256);
+    if (kvcall) {
+      uint64_t ring_in = 0;
+      for (const Pending &pd : inflow) ring_in += pd.fam.bytes();
+      used += std::min<uint64_t>(kRingSlots * kRingSlotMax, align_up(ring_in, 256));
+      used += uint64_t(P.kv.num_blocks) * 12 + 1024;
+    }
+    used += (uint64_t(nodes.size()) * 2 + outbound.size() + inflow.size() + 64) * (sizeof(Desc) + 8) + (1u << 20);
+    tail_room = used < cap ? std::min<uint64_t>(cap - used, kTailMax) : 0;
   }
 
   // ---- in-place dependency graph --------------------------------------------------
@@ -946,6 +976,41 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
           changed = true;
         }
       if (!changed) fail(ATP_ECAPACITY, "in-place schedule: unresolvable order");
+    }
+    // The tail of the level chain through staging.  A shard that grows on
+    // its own arena gives a chain of levels in which each level writes where
+    // the next one reads, each moving about half as much as the one before;
+    // the last levels move little, yet each costs a launch and the gap
+    // before the next one.  The nodes of levels k and above are staged
+    // instead: their reads join level 0 and their writes the level after
+    // the last level that reads their destination, so no level above k
+    // remains.  Every byte so routed is read and written once more.  k
+    // maximises the levels saved times kLevelCost less that extra traffic
+    // at kTailRate, within the room the staging cap leaves.
+    if (tail_room > 0) {
+      int nl = 0;
+      for (int i = 0; i < n; ++i)
+        if (nodes[i].kind == Node::NORMAL) nl = std::max(nl, lvl[i] + 1);
+      std::vector<uint64_t> suffix(size_t(nl) + 1, 0);  // bytes moved by NORMAL nodes of levels >= l
+      for (int i = 0; i < n; ++i)
+        if (nodes[i].kind == Node::NORMAL) suffix[size_t(lvl[i])] += moved_of(nodes[i]);
+      for (int l = nl - 1; l >= 0; --l) suffix[size_t(l)] += suffix[size_t(l) + 1];
+      int best_k = nl;
+      double best_gain = 0;
+      for (int k = 1; k + 1 < nl; ++k) {
+        if (suffix[size_t(k)] > tail_room) continue;
+        const double gain = double(nl - k - 1) * kLevelCost - 2.0 * double(suffix[size_t(k)]) / kTailRate;
+        if (gain > best_gain) {
+          best_gain = gain;
+          best_k = k;
+        }
+      }
+      if (best_k < nl) {
+        for (int i = 0; i < n; ++i)
+          if (nodes[i].kind == Node::NORMAL && lvl[i] >= best_k) nodes[i].kind = Node::STAGED;
+        // fewer NORMAL nodes cannot close a cycle
+        if (!solve(lvl)) fail(ATP_ECAPACITY, "in-place schedule: unresolvable order after staging the tail");
+      }
     }
     for (int i = 0; i < n; ++i) nodes[i].level = lvl[i];
   }
@@ -1153,8 +1218,8 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
     // the 80-layer TP 8->7 reshard in place took 1019.6 ms with 256 MiB
     // slots, 1023.4 with 128 and 1031.6 with 64.
     const uint64_t item = align_up(max_item, 256);
-    auto slots_for = [&](uint64_t s) { return std::min<uint64_t>(4, (ring_total + s - 1) / s); };
-    slot = std::max<uint64_t>(std::min<uint64_t>(256ull << 20, align_up(ring_total, 256)), item);
+    auto slots_for = [&](uint64_t s) { return std::min<uint64_t>(kRingSlots, (ring_total + s - 1) / s); };
+    slot = std::max<uint64_t>(std::min<uint64_t>(kRingSlotMax, align_up(ring_total, 256)), item);
     // respect the staging cap: shrink slots if needed
     while (slots_for(slot) * slot + stage_bytes + (1u << 20) > cap && slot / 2 >= item && slot > (4u << 20))
       slot = align_up(slot / 2, 256);
