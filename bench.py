@@ -38,7 +38,7 @@ COUNTED_TRAFFIC = {
     "src": "98de88c3866af8ac",
     "dense-40L-h5120-tp4to3": {("kv", 10737418240): 10738045781, ("weights", 9043968000): 9069669589},
     "dense-40L-h5120-tp8to7-fragmented-kv": {("kv", 21474836480): 21477139966},
-    "dense-80L-h8192-tp8to7-inplace": {("kv", 42949672960): 42954049916, ("weights", 3460300800): 3460448373},
+    "dense-80L-h8192-tp8to7-inplace": {("kv", 43083890688): 43088211671, ("weights", 3829399552): 3829563243},
 }
 
 
