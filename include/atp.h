@@ -140,9 +140,12 @@ enum {
   ATP_INPLACE = 1 << 4,     /* new layout overwrites the old arena       */
   ATP_PLAN_GREEDY = 1 << 8, /* Sec. V baseline: keep local, reload gaps  */
   ATP_PLAN_FULL = 1 << 9,   /* Sec. V baseline: reload every byte        */
-  ATP_KV_COMPACT = 1 << 10  /* new KV arena holds only the live blocks,  */
+  ATP_KV_COMPACT = 1 << 10, /* new KV arena holds only the live blocks,  */
                             /* block p at its rank among the live ids    */
                             /* (out of place only; see atp_kv_evict_lru) */
+  ATP_NO_TAIL_STAGING = 1 << 11 /* in place: stage only what cycles need,  */
+                            /* never the tail of a level chain (every     */
+                            /* hazard then resolved by levels alone)      */
 };
 
 typedef struct {
@@ -163,7 +166,9 @@ typedef struct atp_plan_obj atp_plan_t;
 
 /* Plan the reshard (Alg. 1 per space, Eq. 1 statistics, Sec. III-C
  * single-pass pre-allocation: new layout sizes and staging needs, and for
- * ATP_INPLACE a hazard-free level order with a bounded staging buffer).
+ * ATP_INPLACE a hazard-free level order with a bounded staging buffer; the
+ * tail of a long level chain goes through the staging the cap leaves when
+ * that saves launches, unless ATP_NO_TAIL_STAGING).
  * Errors: ATP_EINVAL (malformed problem), ATP_ECAPACITY (in-place schedule
  * needs more than staging_cap).  *out is set only on success. */
 int atp_plan(const atp_problem *problem, atp_plan_t **out);
@@ -302,6 +307,8 @@ typedef struct {
   uint64_t staging_w, staging_kv; /* staging bytes each call needs      */
   uint64_t global_keep, global_p2p, global_reload; /* all survivors     */
   uint64_t reload_min;          /* Eq. 1, bytes                         */
+  uint64_t tail_w, tail_kv;     /* of staged: a level chain's tail,     */
+                                /* moved through staging (in place)     */
 } atp_stats;
 int atp_plan_stats(const atp_plan_t *plan, atp_stats *out);
 

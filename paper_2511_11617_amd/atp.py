@@ -27,6 +27,7 @@ INPLACE = 1 << 4
 PLAN_GREEDY = 1 << 8
 PLAN_FULL = 1 << 9
 KV_COMPACT = 1 << 10
+NO_TAIL_STAGING = 1 << 11
 KEEP, P2P, RELOAD = 0, 1, 2
 SEG_INFLOW_W, SEG_OUTBOUND_W, SEG_INFLOW_KV, SEG_OUTBOUND_KV = 0, 1, 2, 3
 
@@ -89,7 +90,7 @@ class Stats(C.Structure):
             "old_arena_bytes", "new_arena_bytes", "old_kv_bytes", "new_kv_bytes",
             "retained_w", "inflow_w", "outbound_w", "retained_kv", "inflow_kv", "outbound_kv",
             "moved_w", "moved_kv", "staged_w", "staged_kv", "staging_w", "staging_kv",
-            "global_keep", "global_p2p", "global_reload", "reload_min")]
+            "global_keep", "global_p2p", "global_reload", "reload_min", "tail_w", "tail_kv")]
 
 
 class Task(C.Structure):

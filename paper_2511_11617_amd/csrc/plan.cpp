@@ -835,7 +835,7 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
   // the landing ring at its full size and the descriptor and block-list
   // area, at most kTailMax.
   uint64_t tail_room = 0;
-  if (P.inplace) {
+  if (P.inplace && !(P.prob.flags & ATP_NO_TAIL_STAGING)) {
     uint64_t used = 0;
     for (const Node &x : nodes)
       if (x.kind != Node::NORMAL) used += align_up(x.kind == Node::GATHER ? x.fam.bytes() : moved_of(x), 256);
@@ -1007,7 +1007,10 @@ void schedule(Plan &P, CallPlan &c, std::vector<Fam> &retained, std::vector<Pend
       }
       if (best_k < nl) {
         for (int i = 0; i < n; ++i)
-          if (nodes[i].kind == Node::NORMAL && lvl[i] >= best_k) nodes[i].kind = Node::STAGED;
+          if (nodes[i].kind == Node::NORMAL && lvl[i] >= best_k) {
+            nodes[i].kind = Node::STAGED;
+            c.tail += moved_of(nodes[i]);
+          }
         // fewer NORMAL nodes cannot close a cycle
         if (!solve(lvl)) fail(ATP_ECAPACITY, "in-place schedule: unresolvable order after staging the tail");
       }
@@ -1381,6 +1384,8 @@ Plan *make_plan(const atp_problem *p) {
   st.moved_kv = P->k.moved;
   st.staged_w = P->w.staged;
   st.staged_kv = P->k.staged;
+  st.tail_w = P->w.tail;
+  st.tail_kv = P->k.tail;
   st.staging_w = P->w.staging_need;
   st.staging_kv = P->has_kv ? P->k.staging_need : 0;
   P->plan_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();

@@ -113,7 +113,7 @@ struct CallPlan {
   std::vector<uint8_t> out_aligned;
   std::vector<atp_segment> seg_in, seg_out;
   int n_levels = 0;
-  uint64_t retained = 0, moved = 0, staged = 0;
+  uint64_t retained = 0, moved = 0, staged = 0, tail = 0;
   uint64_t inflow = 0, outbound_bytes = 0;
   // staging layout
   uint64_t off_meta = 0, off_desc = 0, off_prefix = 0, off_kvflags = 0,

@@ -42,9 +42,11 @@ def test_cfg1_every_survivor(self_old):
     run_case(configs.get(1, self_old=self_old), name="cfg1-survivor")
 
 
+@pytest.mark.parametrize("no_tail", [False, True])
 @pytest.mark.parametrize("layout", ["head", "token"])
-def test_cfg1_in_place(layout):
-    run_case(configs.get(1, kv_layout=layout), flags=atp.INPLACE, name="cfg1-inplace")
+def test_cfg1_in_place(layout, no_tail):
+    flags = atp.INPLACE | (atp.NO_TAIL_STAGING if no_tail else 0)
+    run_case(configs.get(1, kv_layout=layout), flags=flags, name="cfg1-inplace" + ("-levels" if no_tail else ""))
 
 
 @pytest.mark.parametrize("seed", list(range(24)))
@@ -67,15 +69,18 @@ def test_random_medium(seed, mode):
     """Random medium decoders: real 2-4 KiB KV head lines (wide tiles),
     multi-tile weight lines, up to TP 8, fragmented pools."""
     c = med_cfg(random.Random(9000 + seed), experts=seed % 3 == 0)
-    run_case(c, flags=atp.INPLACE if mode == "in-place" else 0, kv_first=mode == "kv-first",
-             name=f"random-medium-{seed}-{mode}")
+    # in place, odd seeds resolve their level chains by levels alone
+    flags = (atp.INPLACE | (atp.NO_TAIL_STAGING if seed % 2 else 0)) if mode == "in-place" else 0
+    run_case(c, flags=flags, kv_first=mode == "kv-first", name=f"random-medium-{seed}-{mode}")
 
 
 @pytest.mark.parametrize("seed", list(range(24)))
 def test_random_small_in_place(seed):
     rng = random.Random(1000 + seed)
     c = tiny_cfg(rng, experts=seed % 3 == 0)
-    run_case(c, flags=atp.INPLACE, name=f"random-inplace-{seed}")
+    # odd seeds resolve their level chains by levels alone
+    flags = atp.INPLACE | (atp.NO_TAIL_STAGING if seed % 2 else 0)
+    run_case(c, flags=flags, name=f"random-inplace-{seed}" + ("-levels" if seed % 2 else ""))
 
 
 @pytest.mark.parametrize("inplace", [False, True])
@@ -99,6 +104,17 @@ def test_in_place_ring_under_a_squeezed_staging_cap():
 def test_cfg5_shape_in_place_two_layers():
     c = configs.scaled(5, layers=2, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
     run_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"], name="cfg5-2layers-inplace")
+
+
+@pytest.mark.parametrize("no_tail", [False, True])
+def test_kv_level_chain_in_place(no_tail):
+    """The 80-layer TP 8 -> 7 workload's KV geometry on a small decoder: the
+    KV shard doubles on its own arena (a chain of about 12 levels), its tail
+    through staging or every level launched."""
+    c = configs.get(5, layers=2, hidden=512, n_q=16, n_kv=8, head_dim=64, ffn=1024, n_seq=8, seq_tokens=1024,
+                    new_q_widths=None, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    flags = atp.INPLACE | (atp.NO_TAIL_STAGING if no_tail else 0)
+    run_case(c, flags=flags, staging_cap=c["staging_cap"], name="kv-chain-inplace" + ("-levels" if no_tail else ""))
 
 
 @pytest.mark.parametrize("variant,flag", [("greedy", atp.PLAN_GREEDY), ("full", atp.PLAN_FULL)])

@@ -78,16 +78,42 @@ def test_cfg1_survivors_in_place(self_old):
 
 
 @settings(max_examples=80, deadline=None)
-@given(st.integers(0, 2 ** 31), st.booleans(), st.booleans())
-def test_random_small(seed, experts, inplace):
+@given(st.integers(0, 2 ** 31), st.booleans(), st.booleans(), st.booleans())
+def test_random_small(seed, experts, inplace, no_tail):
     c = tiny_cfg(random.Random(seed), experts)
-    sim_case(c, flags=atp.INPLACE if inplace else 0)
+    sim_case(c, flags=(atp.INPLACE | (atp.NO_TAIL_STAGING if no_tail else 0)) if inplace else 0)
 
 
 @pytest.mark.parametrize("seed", list(range(10)))
 def test_random_medium(seed):
     c = med_cfg(random.Random(9000 + seed), experts=seed % 3 == 0)
-    sim_case(c, flags=atp.INPLACE if seed % 2 else 0)
+    # in place every other time with the level chains resolved by levels alone
+    sim_case(c, flags=(atp.INPLACE | (atp.NO_TAIL_STAGING if seed % 4 == 1 else 0)) if seed % 2 else 0)
+
+
+def test_level_chain_tail_goes_through_staging():
+    """The 80-layer TP 8 -> 7 workload's KV geometry (one KV head per old
+    rank, two per new one) on a small decoder, in place: the KV shard
+    doubles on its own arena, a chain of levels each moving half as much as
+    the one before.  With room in staging its tail is staged (read in level
+    0, written once its destination is free), leaving few levels; with
+    ATP_NO_TAIL_STAGING the chain is resolved by levels alone.  Both replay
+    to the oracle's bytes, and the tail costs exactly its bytes of staging."""
+    c = configs.get(5, layers=2, hidden=512, n_q=16, n_kv=8, head_dim=64, ffn=1024, n_seq=8, seq_tokens=1024,
+                    new_q_widths=None, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    tail = sim_case(c, flags=atp.INPLACE, staging_cap=c["staging_cap"]).stats()
+    chain = sim_case(c, flags=atp.INPLACE | atp.NO_TAIL_STAGING, staging_cap=c["staging_cap"]).stats()
+    assert chain.tail_w == chain.tail_kv == 0
+    assert chain.n_levels_kv >= 10  # 512 live blocks: a chain of about log2 of them
+    assert tail.tail_kv > 0 and tail.n_levels_kv <= 3
+    assert tail.staged_kv - chain.staged_kv == tail.tail_kv
+    assert tail.moved_kv == chain.moved_kv and tail.moved_w == chain.moved_w
+    # the tail stays within what the cap leaves: a cap at the chain's own
+    # need leaves the KV call no room for it
+    cap = max(chain.staging_w, chain.staging_kv)
+    tight = sim_case(c, flags=atp.INPLACE, staging_cap=cap).stats()
+    assert tight.tail_kv == 0 and tight.n_levels_kv == chain.n_levels_kv
+    assert max(tight.staging_w, tight.staging_kv) <= cap
 
 
 @settings(max_examples=40, deadline=None)
