@@ -371,9 +371,11 @@ def main():
     if evict is not None:
         out["kv_evict"] = evict
     if args.load:
-        def pipelined_step(files, names, buf):
+        def pipelined_step(files, names, buf, deferred=False):
             """One step whose weight inflow is read from the checkpoint while the
-            weights reshard runs behind the reads (atp_load_reshard_weights)."""
+            weights reshard runs behind the reads (atp_load_reshard_weights).
+            `deferred`: atp_load_reshard_weights_async, then the KV call while
+            the reads run, and atp_sync issues the weight pieces."""
             if inplace:
                 fill_old()
             p = built.plan()
@@ -385,13 +387,18 @@ def main():
                              ptr(table_d), table.shape[0], table.shape[1], ptr(hin_k), st.inflow_kv,
                              ptr(hout_k), st.outbound_kv if inplace else 0, ptr(stage_k), stage_k.numel(),
                              compute.cuda_stream, copy.cuda_stream)
-            if not inplace:  # out of place the KV inflow can use the link while the weights are read
+            w_args = (ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0, buf.ptr, st.inflow_w,
+                      ptr(hout_w), st.outbound_w if inplace else 0, ptr(stage_w), stage_w.numel(),
+                      compute.cuda_stream, copy.cuda_stream)
+            if deferred:
+                p.load_reshard_weights_async(files, names, *w_args)
                 kv()
-            p.load_reshard_weights(files, names, ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0,
-                                   buf.ptr, st.inflow_w, ptr(hout_w), st.outbound_w if inplace else 0,
-                                   ptr(stage_w), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
-            if inplace:  # in place the weights call comes first
-                kv()
+            else:
+                if not inplace:  # out of place the KV inflow can use the link while the weights are read
+                    kv()
+                p.load_reshard_weights(files, names, *w_args)
+                if inplace:  # in place the weights call comes first
+                    kv()
             p.sync()
             torch.cuda.synchronize()
             return (time.perf_counter() - t1) * 1e3
@@ -754,32 +761,36 @@ def load_leg(steps, cfg, plan, st, tl, hin_w, Pinned, pipelined_step, step_ms):
                 ms.append(ls.read_ms)
         if not np.array_equal(buf.tensor.numpy(), src):
             raise RuntimeError("range reads returned other bytes than the checkpoint holds")
-        # reads and reshard together: the file reads overlap the landings
-        pipe = []
+        # reads and reshard together: the file reads overlap the landings;
+        # then the same with the reads behind the asynchronous call
+        pipe, defer = [], []
         gc.collect()
         gc.disable()
-        for i in range(steps + 1):  # the first pass is a warm-up
-            buf.tensor.fill_(0xA5)
-            w = pipelined_step(files, names, buf)
-            if i:
-                pipe.append(w)
-            log(f"[bench] reads + reshard pipelined: {w:.1f} ms")
+        for deferred, acc in ((False, pipe), (True, defer)):
+            for i in range(steps + 1):  # the first pass is a warm-up
+                buf.tensor.fill_(0xA5)
+                w = pipelined_step(files, names, buf, deferred)
+                if i:
+                    acc.append(w)
+                log(f"[bench] reads + reshard {'async' if deferred else 'pipelined'}: {w:.1f} ms")
+            if not np.array_equal(buf.tensor.numpy(), src):
+                raise RuntimeError("pipelined range reads returned other bytes than the checkpoint holds")
         gc.enable()
-        if not np.array_equal(buf.tensor.numpy(), src):
-            raise RuntimeError("pipelined range reads returned other bytes than the checkpoint holds")
         files.close()
         buf.close()
     finally:
         shutil.rmtree(d, ignore_errors=True)
     read_ms = sum(ms) / len(ms)
     pipe_ms = sum(pipe) / len(pipe)
+    defer_ms = sum(defer) / len(defer)
     return {"source": f"safetensors range reads, file in {where[0]} (page cache)", "bytes": int(st.inflow_w),
             "tensor_bytes": int(ls.tensor_bytes), "read_fraction": round(st.inflow_w / ls.tensor_bytes, 4),
             "reads": int(ls.reads), "threads": int(ls.threads), "read_ms": round(read_ms, 3),
             "GBps": round(st.inflow_w / (read_ms * 1e-3) / 1e9, 2), "file_bytes": int(total),
             "write_s": round(write_s, 2),
             "sequential_ms": round(read_ms + step_ms, 3),  # reads, then the step from pinned memory
-            "pipelined_ms": round(pipe_ms, 3)}  # reads and reshard together, whole step
+            "pipelined_ms": round(pipe_ms, 3),  # reads and reshard together, whole step
+            "async_ms": round(defer_ms, 3)}  # the same behind atp_load_reshard_weights_async, KV call between
 
 
 def h2d_probe(torch, bufs, max_bytes, stream, chunk=64 << 20):

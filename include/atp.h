@@ -474,6 +474,29 @@ int atp_load_reshard_weights(atp_plan_t *plan, const atp_st_t *st, const char *c
                              atp_stream compute, atp_stream copy, int32_t n_threads,
                              atp_load_stats *stats);
 
+/* The same pipelined reload, returning before the reads are done (Sec.
+ * III-C: the reloads overlap the rest of the recovery, the KV move
+ * included).  Queues the work that needs no inflow byte (prepare, outbound
+ * reads, repack levels) and starts the reads; the inflow pieces are issued
+ * by atp_sync, each once the reads under it have completed, and atp_sync
+ * returns once they have landed.  Between the two calls the caller may
+ * issue atp_reshard_kv (in place this is the order the library needs, and
+ * its KV inflow then uses the link while the weights are read).  `st`,
+ * `names` and every buffer must stay valid until atp_sync returns.  Name or
+ * shape errors are ATP_EINVAL before anything starts; a failed read is
+ * atp_sync's ATP_EINVAL, after the queued work has drained.  The read
+ * statistics come from atp_plan_load_stats after atp_sync. */
+int atp_load_reshard_weights_async(atp_plan_t *plan, const atp_st_t *st, const char *const *names,
+                                   int32_t n_names, void *arena, uint64_t arena_bytes,
+                                   void *new_arena, uint64_t new_arena_bytes,
+                                   void *inflow_host, uint64_t inflow_bytes,
+                                   void *outbound_host, uint64_t outbound_bytes,
+                                   void *staging, uint64_t staging_bytes,
+                                   atp_stream compute, atp_stream copy, int32_t n_threads);
+/* Read statistics of the plan's last atp_load_reshard_weights_async, once
+ * atp_sync has returned ATP_OK for it; ATP_ESTATE before. */
+int atp_plan_load_stats(const atp_plan_t *plan, atp_load_stats *out);
+
 /* ---- KV budget under recovery (Sec. III-A: per-session recency; cold KV
  * released least recently used first when the demand exceeds the budget,
  * evicted sessions being rebuilt later by replay) ----------------------- */

@@ -39,7 +39,7 @@ EXPORTS = [
     "atp_kv_evict_lru", "atp_daemon_serve", "atp_state_connect", "atp_state_disconnect",
     "atp_state_alloc", "atp_state_open", "atp_state_release", "atp_state_free", "atp_state_put",
     "atp_state_get", "atp_state_list", "atp_state_shutdown", "atp_warmup", "atp_load_reshard_weights",
-    "atp_reshard_kv_noalloc", "atp_scratch_bytes",
+    "atp_reshard_kv_noalloc", "atp_scratch_bytes", "atp_load_reshard_weights_async", "atp_plan_load_stats",
 ]
 
 
@@ -181,6 +181,10 @@ def _load():
     lib.atp_load_reshard_weights.argtypes = [P, P, C.POINTER(C.c_char_p), C.c_int32, P, C.c_uint64, P,
                                              C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, P,
                                              C.c_int32, C.POINTER(LoadStats)]
+    lib.atp_load_reshard_weights_async.argtypes = [P, P, C.POINTER(C.c_char_p), C.c_int32, P, C.c_uint64, P,
+                                                   C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, C.c_uint64, P, P,
+                                                   C.c_int32]
+    lib.atp_plan_load_stats.argtypes = [P, C.POINTER(LoadStats)]
     lib.atp_kv_evict_lru.argtypes = [P, C.c_int32, C.c_int32, C.c_int64, P, C.c_uint64, C.c_uint64, C.c_int32,
                                      P, P, C.POINTER(EvictStats)]
     lib.atp_daemon_serve.argtypes = [C.c_char_p, C.c_int32]
@@ -334,6 +338,23 @@ class Plan:
         _check(lib.atp_load_reshard_weights(self.h, files.h, arr, len(names), arena, arena_bytes, new_arena,
                                             new_bytes, inflow, inflow_bytes, outbound, outbound_bytes, staging,
                                             staging_bytes, compute, copy, threads, C.byref(st)))
+        return st
+
+    def load_reshard_weights_async(self, files: "StFiles", names, arena, arena_bytes, new_arena, new_bytes, inflow,
+                                   inflow_bytes, outbound, outbound_bytes, staging, staging_bytes, compute, copy,
+                                   threads=0) -> None:
+        """The same reload, returning before the reads are done: the inflow
+        pieces are issued by sync(); `files`, the names and every buffer stay
+        valid until then (the ctypes array of names is kept here)."""
+        self._names = (C.c_char_p * len(names))(*[n.encode() for n in names])
+        self._files = files
+        _check(lib.atp_load_reshard_weights_async(self.h, files.h, self._names, len(names), arena, arena_bytes,
+                                                  new_arena, new_bytes, inflow, inflow_bytes, outbound,
+                                                  outbound_bytes, staging, staging_bytes, compute, copy, threads))
+
+    def load_stats(self) -> LoadStats:
+        st = LoadStats()
+        _check(lib.atp_plan_load_stats(self.h, C.byref(st)))
         return st
 
 

@@ -376,6 +376,38 @@ int atp_load_reshard_weights(atp_plan_t *plan, const atp_st_t *st, const char *c
   });
 }
 
+int atp_load_reshard_weights_async(atp_plan_t *plan, const atp_st_t *st, const char *const *names,
+                                   int32_t n_names, void *arena, uint64_t arena_bytes, void *new_arena,
+                                   uint64_t new_arena_bytes, void *inflow_host, uint64_t inflow_bytes,
+                                   void *outbound_host, uint64_t outbound_bytes, void *staging, uint64_t staging_bytes,
+                                   atp_stream compute, atp_stream copy, int32_t n_threads) {
+  return guard([&]() -> int {
+    if (!plan || !st) return fail(ATP_EINVAL, "plan or st is NULL");
+    atp::Plan *P = plan->p;
+    // checks the names and builds the reads before anything starts; the job
+    // lives until atp_sync has issued every piece (or the plan is freed)
+    auto job = std::make_shared<atp::LoadJob>(*P, *st->f, names, n_names, inflow_host, inflow_bytes, n_threads);
+    job->start();
+    P->load_stats_valid = false;
+    const std::function<void(uint64_t)> await = [job](uint64_t end) { job->await(end); };
+    atp::exec_call(*P, false, arena, arena_bytes, new_arena, new_arena_bytes, inflow_host, inflow_bytes,
+                   outbound_host, outbound_bytes, nullptr, 0, staging, staging_bytes,
+                   static_cast<hipStream_t>(compute), static_cast<hipStream_t>(copy), &await, false, true,
+                   [job, P]() {
+                     job->finish(&P->load_stats);
+                     P->load_stats_valid = true;
+                   });
+    return ATP_OK;
+  });
+}
+
+int atp_plan_load_stats(const atp_plan_t *plan, atp_load_stats *out) {
+  if (!plan || !out) return fail(ATP_EINVAL, "NULL argument");
+  if (!plan->p->load_stats_valid) return fail(ATP_ESTATE, "no synced atp_load_reshard_weights_async on this plan");
+  *out = plan->p->load_stats;
+  return ATP_OK;
+}
+
 int atp_kv_evict_lru(const int32_t *table, int32_t n_seq, int32_t max_blocks, int64_t num_blocks,
                      const int64_t *last_use, uint64_t block_bytes, uint64_t budget_bytes, int32_t compact,
                      int32_t *keep, int32_t *new_table, atp_evict_stats *stats) {

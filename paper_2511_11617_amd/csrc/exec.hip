@@ -14,6 +14,7 @@
 #include <algorithm>
 #include <chrono>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <cstdio>
 #include <cstring>
@@ -68,6 +69,10 @@ struct CallState {
   };
   std::vector<LaunchRec> launches;
   uint64_t h2d_bytes = 0, d2h_bytes = 0, scatter_bytes = 0, repack_bytes = 0;
+  hipStream_t compute = nullptr, copy = nullptr;  // the caller's streams of the pending call
+  // A weights call whose inflow buffer is still being read: its awaited
+  // pieces are issued by atp_sync (then the tails are recorded again).
+  std::function<void()> finish_issue;
 };
 
 // Process-wide recycling of HIP objects per device.  Each plan owns what it
@@ -435,6 +440,119 @@ void launch_copy(Exec &E, const Launch &L, const Desc *dev_desc, const int64_t *
   HIPCHK(hipGetLastError());
 }
 
+// ---- issuing one call ----------------------------------------------------------------
+// Every event recorded on a stream costs it a few microseconds (about 4.5 us
+// each on the MI355X, against 2 us between two bare launches), so the
+// launches of a stream share their timing marks: a launch that comes right
+// after a timed one starts at that launch's end mark, and the events other
+// streams wait on are those same marks.  mark[s] is the end mark of the last
+// command queued on s when that command was a timed launch; other(s) forgets
+// it when anything else is queued there.  The Issuer also lands the inflow
+// pieces that are not repack: DMA copies of large gaps and the copy kernel's
+// reads of the pinned host buffer.  A deferred issue (the weights call of
+// atp_load_reshard_weights_async) keeps a copy of it, with marks of its own.
+struct Issuer {
+  Exec &E;
+  CallState &cs;
+  const CallPlan &c;
+  int64_t nb, live;  // KV pool size and live blocks (0 for the weights call)
+  char *b_out, *b_st;
+  const char *host_in;
+  Desc *dev_desc;
+  int64_t *dev_prefix;
+  int32_t *dev_live;
+  hipStream_t copy;
+  std::map<hipStream_t, hipEvent_t> mark;
+
+  void other(hipStream_t st) { mark.erase(st); }
+  void record(hipEvent_t e, hipStream_t st) {
+    HIPCHK(hipEventRecord(e, st));
+    other(st);
+  }
+  template <class F>
+  CallState::LaunchRec timed(int kind, int level, uint64_t bytes, hipStream_t st, const F &launch) {
+    CallState::LaunchRec r{kind, level, bytes, nullptr, E.ev_time()};
+    auto it = mark.find(st);
+    if (it != mark.end()) {
+      r.e0 = it->second;
+    } else {
+      r.e0 = E.ev_time();
+      HIPCHK(hipEventRecord(r.e0, st));
+    }
+    launch();
+    HIPCHK(hipEventRecord(r.e1, st));
+    mark[st] = r.e1;
+    cs.launches.push_back(r);
+    return r;
+  }
+  // an event that fires once everything queued on st so far is done: the
+  // last end mark there, or a fresh event (a fresh timing event is then the
+  // mark a following launch starts at)
+  hipEvent_t mark_or_record(hipStream_t st, bool timing) {
+    auto it = mark.find(st);
+    if (it != mark.end()) return it->second;
+    hipEvent_t e = timing ? E.ev_time() : E.ev_sync();
+    HIPCHK(hipEventRecord(e, st));
+    if (timing) mark[st] = e;
+    return e;
+  }
+  // a large contiguous gap straight into place by DMA
+  void direct(const HostCopy &h) {
+    HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
+    cs.h2d_bytes += h.bytes;
+  }
+  // the copy kernel reads inflow pieces from the pinned host buffer into
+  // their final place (kind 4 launches)
+  void host_read(const Launch &L, hipStream_t s) {
+    timed(4, -1, L.bytes, s, [&] {
+      launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s, kHostReadGrid);
+    });
+    cs.h2d_bytes += L.bytes;
+  }
+  void end_host_reads(hipStream_t s) { cs.hr1 = mark_or_record(s, true); }
+  // While the inflow buffer is still being filled, the direct landings and
+  // the host reads (each launch cut at descriptor boundaries into pieces of
+  // at least kPipeBytes) are issued in the order of the end of the bytes
+  // they read, each once `await` says those bytes are in.
+  void awaited(hipStream_t s, const std::function<void(uint64_t)> &await) {
+    struct Piece {
+      uint64_t end;
+      const HostCopy *direct;
+      Launch L;
+    };
+    std::vector<Piece> pieces;
+    for (const HostCopy &h : c.directs) pieces.push_back({h.host_off + h.bytes, &h, Launch{}});
+    for (const Launch &L : c.host_reads) {
+      Launch piece = L;
+      piece.bytes = 0;
+      uint64_t end = 0;
+      for (int d = L.d0; d < L.d1; ++d) {
+        const Fam &f = c.fams[size_t(d)];
+        piece.bytes += (f.o_end - f.o_begin) * f.rows * f.run;
+        end = std::max(end, extent(f, true, nb, live));  // source side: the inflow buffer
+        if (piece.bytes >= kPipeBytes || d + 1 == L.d1) {
+          piece.d1 = d + 1;
+          pieces.push_back({end, nullptr, piece});
+          piece.d0 = d + 1;
+          piece.bytes = 0;
+          end = 0;
+        }
+      }
+    }
+    std::stable_sort(pieces.begin(), pieces.end(), [](const Piece &x, const Piece &y) { return x.end < y.end; });
+    for (const Piece &x : pieces) {
+      await(x.end);
+      if (x.direct) {
+        direct(*x.direct);
+      } else {
+        other(s);  // the launch starts once the host has waited: it gets a start mark of its own
+        host_read(x.L, s);
+      }
+    }
+    if (!c.host_reads.empty()) end_host_reads(s);
+  }
+};
+
 // ---- the scratch array of the no-allocation entry point --------------------------
 // Callers that cannot allocate (code under HIP graph capture, tight serving
 // loops) reshard on this file-scope device array instead of a staging
@@ -471,8 +589,10 @@ uint64_t scratch_bytes() { return kScratchBytes; }
 void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *new_arena, uint64_t new_bytes,
                const void *inflow_host, uint64_t inflow_bytes, void *outbound_host, uint64_t outbound_bytes,
                const int32_t *table, int64_t n_entries, void *staging, uint64_t staging_bytes, hipStream_t compute,
-               hipStream_t copy, const std::function<void(uint64_t)> *await, bool on_scratch) {
+               hipStream_t copy, const std::function<void(uint64_t)> *await, bool on_scratch, bool defer,
+               std::function<void()> after_issue) {
   CallPlan &c = kvcall ? P.k : P.w;
+  if (defer && (!await || kvcall)) throw Error(ATP_EINVAL, "internal: only a weights call that awaits its inflow is deferred");
   if (on_scratch) {
     // the device's scratch array in place of a staging buffer
     if (c.staging_need > kScratchBytes)
@@ -605,45 +725,11 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   int32_t *dev_err = reinterpret_cast<int32_t *>(b_st + c.off_meta);
   int32_t *dev_live = kvcall ? reinterpret_cast<int32_t *>(b_st + c.off_kvlive) : nullptr;
 
-  // Every event recorded on a stream costs it a few microseconds (about
-  // 4.5 us each on the MI355X, against 2 us between two bare launches), so
-  // the launches of a stream share their timing marks: a launch that comes
-  // right after a timed one starts at that launch's end mark, and the
-  // events other streams wait on are those same marks.  mark[s] is the end
-  // mark of the last command queued on s when that command was a timed
-  // launch; `other(s)` forgets it when anything else is queued there.
-  std::map<hipStream_t, hipEvent_t> mark;
-  auto other = [&](hipStream_t st) { mark.erase(st); };
-  auto record = [&](hipEvent_t e, hipStream_t st) {
-    HIPCHK(hipEventRecord(e, st));
-    other(st);
-  };
-  auto timed = [&](int kind, int level, uint64_t bytes, hipStream_t st, const auto &launch) {
-    CallState::LaunchRec r{kind, level, bytes, nullptr, E.ev_time()};
-    auto it = mark.find(st);
-    if (it != mark.end()) {
-      r.e0 = it->second;
-    } else {
-      r.e0 = E.ev_time();
-      HIPCHK(hipEventRecord(r.e0, st));
-    }
-    launch();
-    HIPCHK(hipEventRecord(r.e1, st));
-    mark[st] = r.e1;
-    cs.launches.push_back(r);
-    return r;
-  };
-  // an event that fires once everything queued on st so far is done: the
-  // last end mark there, or a fresh event (a fresh timing event is then the
-  // mark a following launch starts at)
-  auto mark_or_record = [&](hipStream_t st, bool timing) {
-    auto it = mark.find(st);
-    if (it != mark.end()) return it->second;
-    hipEvent_t e = timing ? E.ev_time() : E.ev_sync();
-    HIPCHK(hipEventRecord(e, st));
-    if (timing) mark[st] = e;
-    return e;
-  };
+  Issuer is{E, cs, c, kvcall ? P.kv.num_blocks : 0, kvcall ? P.kv.live_blocks : 0, b_out, b_st, host_in,
+            dev_desc, dev_prefix, dev_live, copy, {}};
+  cs.compute = compute;
+  cs.copy = copy;
+  cs.finish_issue = nullptr;
 
   // The side stream runs, in place, the weights call's outbound reads,
   // levels and host reads and the KV call's outbound copies; out of place,
@@ -669,12 +755,8 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // so that the host does not wait for the reads before the repack is queued.
   cs.h2d0 = E.ev_time();
   HIPCHK(hipEventRecord(cs.h2d0, copy));
-  auto issue_direct = [&](const HostCopy &h) {
-    HIPCHK(hipMemcpyAsync(b_out + h.dev_off, host_in + h.host_off, h.bytes, hipMemcpyHostToDevice, copy));
-    cs.h2d_bytes += h.bytes;
-  };
   if (!await)
-    for (const HostCopy &h : c.directs) issue_direct(h);
+    for (const HostCopy &h : c.directs) is.direct(h);
 
   // ---- upload descriptors, prepare ----------------------------------------------
   if (!c.fams.empty())
@@ -697,73 +779,22 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   // k_prepare is the only writer of the error word: it stores it once
   hipLaunchKernelGGL(k_prepare, dim3(1), dim3(1024), 0, compute, pa);
   HIPCHK(hipGetLastError());
-  other(compute);
+  is.other(compute);
   hipEvent_t prepared = nullptr;  // descriptors, prefix sums and live blocks in place
   if (use_side) {
     prepared = E.ev_sync();
-    record(prepared, compute);
+    is.record(prepared, compute);
   }
 
-  // the copy kernel reads inflow pieces from the pinned host buffer into
-  // their final place (kind 4 launches)
-  auto host_read = [&](const Launch &L, hipStream_t s) {
-    timed(4, -1, L.bytes, s, [&] {
-      launch_copy(E, L, dev_desc, dev_prefix, const_cast<char *>(host_in), b_out, b_st, dev_live, s, kHostReadGrid);
-    });
-    cs.h2d_bytes += L.bytes;
-  };
-  auto end_host_reads = [&](hipStream_t s) { cs.hr1 = mark_or_record(s, true); };
-  // While the inflow buffer is still being filled (`await`), the direct
-  // landings and the host reads (each launch cut at descriptor boundaries
-  // into pieces of at least kPipeBytes) are issued in the order of the end
-  // of the bytes they read, each once those bytes are in.
-  auto issue_awaited = [&](hipStream_t s) {
-    struct Piece {
-      uint64_t end;
-      const HostCopy *direct;
-      Launch L;
-    };
-    std::vector<Piece> pieces;
-    for (const HostCopy &h : c.directs) pieces.push_back({h.host_off + h.bytes, &h, Launch{}});
-    const int64_t nb = kvcall ? P.kv.num_blocks : 0, live = kvcall ? P.kv.live_blocks : 0;
-    for (const Launch &L : c.host_reads) {
-      Launch piece = L;
-      piece.bytes = 0;
-      uint64_t end = 0;
-      for (int d = L.d0; d < L.d1; ++d) {
-        const Fam &f = c.fams[size_t(d)];
-        piece.bytes += (f.o_end - f.o_begin) * f.rows * f.run;
-        end = std::max(end, extent(f, true, nb, live));  // source side: the inflow buffer
-        if (piece.bytes >= kPipeBytes || d + 1 == L.d1) {
-          piece.d1 = d + 1;
-          pieces.push_back({end, nullptr, piece});
-          piece.d0 = d + 1;
-          piece.bytes = 0;
-          end = 0;
-        }
-      }
-    }
-    std::stable_sort(pieces.begin(), pieces.end(), [](const Piece &x, const Piece &y) { return x.end < y.end; });
-    for (const Piece &x : pieces) {
-      (*await)(x.end);
-      if (x.direct) {
-        issue_direct(*x.direct);
-      } else {
-        other(s);  // the launch starts once the host has waited: it gets a start mark of its own
-        host_read(x.L, s);
-      }
-    }
-    if (!c.host_reads.empty()) end_host_reads(s);
-  };
   cs.hr1 = nullptr;
   // out of place: at once, on the side stream, beside the repack (the two
   // write disjoint bytes of the new arena)
   if (early_reads) {
     HIPCHK(hipStreamWaitEvent(E.side, prepared, 0));
-    other(E.side);
+    is.other(E.side);
     if (!await) {
-      for (const Launch &L : c.host_reads) host_read(L, E.side);
-      end_host_reads(E.side);
+      for (const Launch &L : c.host_reads) is.host_read(L, E.side);
+      is.end_host_reads(E.side);
     }
   }
 
@@ -781,7 +812,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
   if (split) {
     late_comp = E.side;  // the outbound launches read the descriptors
     HIPCHK(hipStreamWaitEvent(late_comp, prepared, 0));
-    other(late_comp);
+    is.other(late_comp);
   }
   std::vector<size_t> pos_of(c.outbound.size(), 0);
   for (size_t p = 0; p < c.out_order.size(); ++p) pos_of[size_t(c.out_order[p])] = p;
@@ -797,7 +828,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
         L.bytes += c.outbound[size_t(c.out_order[issued])].bytes;
       }
       L.d1 = c.out_d0 + int(issued);
-      const CallState::LaunchRec r = timed(3, -1, L.bytes, late_comp, [&] {
+      const CallState::LaunchRec r = is.timed(3, -1, L.bytes, late_comp, [&] {
         launch_copy(E, L, dev_desc, dev_prefix, b_in, host_out, b_st, dev_live, late_comp, kOutboundGrid);
       });
       if (!cs.d2h0) cs.d2h0 = r.e0;
@@ -817,7 +848,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
       for (int o : L.wait_outbound) need = std::max(need, pos_of[size_t(o)] + 1);
       issue_outbound(need);
     }
-    const CallState::LaunchRec r = timed(kvcall ? 1 : 0, L.level, L.bytes, late_comp, [&] {
+    const CallState::LaunchRec r = is.timed(kvcall ? 1 : 0, L.level, L.bytes, late_comp, [&] {
       launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp);
     });
     if (!cs.rep0) cs.rep0 = r.e0;
@@ -825,31 +856,32 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     if (L.level == 0) level0_end = r.e1;
   }
   if (split) issue_outbound(c.out_order.size());  // pieces no level waits for
-  if (!cs.rep0) cs.rep0 = mark_or_record(late_comp, true);
-  cs.rep1 = mark_or_record(late_comp, true);  // also: prepare and every level are done
+  if (!cs.rep0) cs.rep0 = is.mark_or_record(late_comp, true);
+  cs.rep1 = is.mark_or_record(late_comp, true);  // also: prepare and every level are done
 
   // in place: the copy kernel reads every gated or strided inflow piece from
   // the pinned host buffer into its final place, after the last level (and,
   // for the weights, after every outbound read)
-  if (await) {
-    issue_awaited(P.inplace ? late_comp : E.side);
-  } else if (P.inplace && !c.host_reads.empty()) {
-    for (const Launch &L : c.host_reads) host_read(L, late_comp);
-    end_host_reads(late_comp);
+  const hipStream_t await_stream = P.inplace ? late_comp : E.side;
+  if (await && !defer) {
+    is.awaited(await_stream, *await);
+  } else if (!await && P.inplace && !c.host_reads.empty()) {
+    for (const Launch &L : c.host_reads) is.host_read(L, late_comp);
+    is.end_host_reads(late_comp);
   }
 
   // KV outbound gathered into staging at level 0: copy it out after that level
   if (do_out && kvcall) {
     if (level0_end) HIPCHK(hipStreamWaitEvent(E.side, level0_end, 0));
     cs.d2h0 = E.ev_time();
-    record(cs.d2h0, E.side);
+    is.record(cs.d2h0, E.side);
     for (size_t o = 0; o < c.outbound.size(); ++o) {
       const HostCopy &h = c.outbound[o];
       HIPCHK(hipMemcpyAsync(host_out + h.host_off, b_st + h.dev_off, h.bytes, hipMemcpyDeviceToHost, E.side));
       cs.d2h_bytes += h.bytes;
     }
     cs.d2h1 = E.ev_time();
-    record(cs.d2h1, E.side);
+    is.record(cs.d2h1, E.side);
   }
 
   // ---- inflow ------------------------------------------------------------------------
@@ -870,13 +902,13 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     hipEvent_t landed = E.ev_sync();
     HIPCHK(hipEventRecord(landed, copy));
     HIPCHK(hipStreamWaitEvent(late_comp, landed, 0));
-    other(late_comp);
+    is.other(late_comp);
     for (const Launch &L : ch.scatters) {
-      timed(2, -1, L.bytes, late_comp,
-            [&] { launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp); });
+      is.timed(2, -1, L.bytes, late_comp,
+               [&] { launch_copy(E, L, dev_desc, dev_prefix, b_in, b_out, b_st, dev_live, late_comp); });
       cs.scatter_bytes += L.bytes;
     }
-    slot_free[i] = mark_or_record(late_comp, false);  // the chunk's last scatter is done
+    slot_free[i] = is.mark_or_record(late_comp, false);  // the chunk's last scatter is done
   }
   cs.h2d1 = E.ev_time();  // the inflow ends with the later of this and hr1
   HIPCHK(hipEventRecord(cs.h2d1, copy));
@@ -893,6 +925,30 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     // would hold up the other call's work); atp_sync waits for it
     cs.tail_side = E.ev_sync();
     HIPCHK(hipEventRecord(cs.tail_side, E.side));
+  }
+  if (defer) {
+    // the awaited pieces wait for the reads: atp_sync issues them (the
+    // caller may queue the KV call meanwhile), then records the tails again
+    auto d = std::make_shared<Issuer>(is);
+    d->mark.clear();
+    const std::function<void(uint64_t)> aw = *await;
+    const hipStream_t side = use_side ? E.side : nullptr;
+    cs.finish_issue = [d, aw, after_issue, await_stream, compute, copy, side]() {
+      Exec &E = d->E;
+      CallState &cs = d->cs;
+      d->awaited(await_stream, aw);
+      cs.h2d1 = E.ev_time();
+      HIPCHK(hipEventRecord(cs.h2d1, copy));
+      cs.tail_compute = E.ev_sync();
+      HIPCHK(hipEventRecord(cs.tail_compute, compute));
+      cs.tail_copy = E.ev_sync();
+      HIPCHK(hipEventRecord(cs.tail_copy, copy));
+      if (side) {
+        cs.tail_side = E.ev_sync();
+        HIPCHK(hipEventRecord(cs.tail_side, side));
+      }
+      if (after_issue) after_issue();
+    };
   }
   cs.pending = true;
   undo.armed = false;
@@ -911,6 +967,25 @@ int exec_sync(Plan &P, atp_timing *out) {
     if (a && b && hipEventElapsedTime(&f, a, b) == hipSuccess) return double(f);
     return 0.0;
   };
+  // a deferred issue first: its pieces wait for the reads, then its tails
+  // are recorded again; if it fails (a read, a HIP call), everything the
+  // plan queued drains before the error is returned
+  for (CallState *c : {&E.w, &E.k}) {
+    if (!c->pending || !c->finish_issue) continue;
+    std::function<void()> f = std::move(c->finish_issue);
+    c->finish_issue = nullptr;
+    try {
+      f();
+    } catch (const std::exception &e) {
+      if (rc == ATP_OK) {
+        const Error *ae = dynamic_cast<const Error *>(&e);
+        rc = ae ? ae->code : ATP_EINVAL;
+        msg = e.what();
+      }
+      for (hipStream_t s : {c->compute, c->copy, E.side})
+        if (s && hipStreamSynchronize(s) != hipSuccess) (void)hipGetLastError();
+    }
+  }
   double h2d_ms = 0, rep_ms = 0;
   hipEvent_t h2d_first = nullptr, h2d_last = nullptr;  // union span of both calls
   const bool was_pending[2] = {E.w.pending, E.k.pending};
@@ -1002,6 +1077,7 @@ void exec_free(Plan &P) {
       if (c->pending)
         for (hipEvent_t e : {c->tail_compute, c->tail_copy, c->tail_side})
           if (e) (void)hipEventSynchronize(e);
+      c->finish_issue = nullptr;  // a deferred issue never run: its readers stop and join
       release_scratch(*E, *c);
     }
     delete E;

@@ -143,6 +143,9 @@ struct Plan {
   double plan_ms = 0;
 
   void *exec = nullptr;  // executor state (exec.hip)
+  // read statistics of the last atp_load_reshard_weights_async, once synced
+  atp_load_stats load_stats{};
+  bool load_stats_valid = false;
 };
 
 // Build a plan; throws Error.

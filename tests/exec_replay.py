@@ -3,7 +3,10 @@ libatp.so with the HIP runtime replaced by tests/mockhip (preloaded), and
 prints one line per case.  No torch, no GPU.
 
 argv: a JSON list of cases {"w": workload, "inplace": bool, "order":
-"weights-first" | "kv-first", "steps": n, "warmup": bool}.
+"weights-first" | "kv-first" | "async-load", "steps": n, "warmup": bool,
+"layers": optional layer count}.  "async-load" reads the weight inflow
+from a checkpoint of holes (atp_load_reshard_weights_async), issues the KV
+call while the reads run and lets atp_sync issue the weight pieces.
 """
 import ctypes as C
 import json
@@ -17,7 +20,7 @@ mock = C.CDLL(os.environ["ATP_MOCKHIP"])
 import numpy as np  # noqa: E402
 
 from paper_2511_11617_amd import atp, problem  # noqa: E402
-from synth import configs, pagetable  # noqa: E402
+from synth import checkpoint, configs, pagetable  # noqa: E402
 
 
 def dmalloc(n):
@@ -40,6 +43,8 @@ def stream():
 
 def run(case):
     c = configs.get(case["w"], inplace=case["inplace"])
+    if case.get("layers"):
+        c["layers"] = case["layers"]
     table, pool = pagetable.make_for(c)
     n_live = len(np.unique(table[table >= 0]))
     inplace = bool(c["inplace"])
@@ -58,6 +63,13 @@ def run(case):
     s0, s1 = stream(), stream()
     if case["warmup"]:
         atp.warmup(s0, s1, 256)
+    files = names = None
+    if case["order"] == "async-load":
+        tl = problem.tensor_list(c)
+        path = os.path.join(os.environ["ATP_REPLAY_TMP"], f"w{case['w']}.safetensors")
+        checkpoint.write_stream(path, [(n, l, r, cc) for (n, l, k, sp, r, cc, u) in tl], [])
+        files = atp.StFiles([path])
+        names = [checkpoint.name(n, l) for (n, l, *_) in tl]
     launches = []
     for _ in range(case["steps"]):
         p = b.plan()
@@ -75,6 +87,11 @@ def run(case):
             if case["order"] == "kv-first":
                 kcall()
                 wcall()
+            elif case["order"] == "async-load":
+                p.load_reshard_weights_async(files, names, aw, aw_n, nw, st.new_arena_bytes if nw else 0, hin_w,
+                                             st.inflow_w, hout_w, st.outbound_w if inplace else 0, sw,
+                                             max(st.staging_w, 256), s0, s1)
+                kcall()
             else:
                 wcall()
                 kcall()
@@ -82,6 +99,8 @@ def run(case):
             p.sync()
             return {"refused": e.code, "msg": str(e)}
         t = p.sync()
+        if case["order"] == "async-load":
+            assert p.load_stats().bytes == st.inflow_w
         launches.append(int(t.n_launches))
     return {"ok": True, "launches": launches, "mock_launches": int(mock.mock_launches()),
             "mock_copies": int(mock.mock_copies()), "streams": int(mock.mock_streams())}

@@ -73,6 +73,9 @@ def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=Tru
     written there by the library's range-read loader instead of being copied
     from the oracle's packed inflow; with `pipelined` too, the reads and the
     weights reshard run together (atp_load_reshard_weights).  A
+    `pipelined="async"` the reads run behind atp_load_reshard_weights_async:
+    the KV call is issued while they run and atp_sync issues the weight
+    pieces as the reads complete.  A
     `sparse_ckpt` holds only the intervals the plan reads (the oracle's
     packed inflow put back at its tensor coordinates), holes elsewhere.
     `kv_first` issues the KV call before the weights call (out of place
@@ -185,8 +188,12 @@ def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=Tru
     w_args = (ptr(aw), aw.numel(), ptr(nw), nw.numel() if nw is not None else 0, ptr(hin_w), in_w.size,
               ptr(hout_w), st.outbound_w, ptr(stage_w), stage_w.numel(), compute.cuda_stream, copy.cuda_stream)
 
+    deferred = ckpt_dir is not None and in_w.size and pipelined == "async"
+
     def weights_call():
-        if ckpt_dir is not None and in_w.size and pipelined:
+        if deferred:
+            plan.load_reshard_weights_async(files, ckpt_names, *w_args)
+        elif ckpt_dir is not None and in_w.size and pipelined:
             ls = plan.load_reshard_weights(files, ckpt_names, *w_args)
             assert ls.bytes == in_w.size
             files.close()
@@ -212,6 +219,9 @@ def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=Tru
     def finish():
         t = plan.sync()
         torch.cuda.synchronize()
+        if deferred:
+            assert plan.load_stats().bytes == in_w.size
+            files.close()
         got_w = (aw if inplace else nw).cpu().numpy()[:want_w.size]
         got_k = (ak if inplace else nk).cpu().numpy()[:want_k.size]
         bad_w = np.flatnonzero(got_w[mask_w] != want_w[mask_w])

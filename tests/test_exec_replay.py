@@ -27,8 +27,10 @@ def mockhip(tmp_path_factory):
     return out
 
 
-def _replay(mockhip, cases):
+def _replay(mockhip, cases, tmp=None):
     env = dict(os.environ)
+    if tmp is not None:
+        env["ATP_REPLAY_TMP"] = str(tmp)
     # appended, so that anything already preloaded stays first
     env["LD_PRELOAD"] = ":".join(x for x in (env.get("LD_PRELOAD", ""), mockhip) if x)
     env["ATP_MOCKHIP"] = mockhip
@@ -60,3 +62,15 @@ def test_in_place_weights_first_and_kv_first_refused(mockhip):
     assert [r.get("ok") for r in res[:3]] == [True] * 3
     assert res[0]["launches"][0] > 100  # 22 weight and 25 KV levels, outbound reads, ring scatters
     assert res[3]["refused"] == -5 and "before" in res[3]["msg"]
+
+
+def test_async_load_with_the_kv_call_between(mockhip, tmp_path):
+    """atp_load_reshard_weights_async, the KV call while the reads run, then
+    atp_sync issuing the weight pieces: in and out of place, fresh plans in
+    a row, with the reads from a checkpoint of holes."""
+    cases = [{"w": 1, "inplace": False, "order": "async-load", "steps": 2, "warmup": False},
+             {"w": 1, "inplace": True, "order": "async-load", "steps": 2, "warmup": True},
+             {"w": 2, "inplace": False, "order": "async-load", "steps": 2, "warmup": False, "layers": 1},
+             {"w": 2, "inplace": True, "order": "async-load", "steps": 2, "warmup": False, "layers": 1}]
+    res = _replay(mockhip, cases, tmp_path)
+    assert [r.get("ok") for r in res] == [True] * 4, res
