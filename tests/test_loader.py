@@ -167,6 +167,14 @@ def test_missing_and_mismatched_tensors(tmp_path):
                                                      *no_gpu, None, None), "one tensor name")
     _expect_einval(lambda: plan.load_reshard_weights(files, swapped, 0, 0, 0, 0, buf.ctypes.data, n_in,
                                                      *no_gpu, None, None), "shape")
+    # and so does the asynchronous one; nothing is pending after the refusal
+    _expect_einval(lambda: plan.load_reshard_weights_async(files, names[:-1], 0, 0, 0, 0, buf.ctypes.data, n_in,
+                                                           *no_gpu, None, None), "one tensor name")
+    _expect_einval(lambda: plan.load_reshard_weights_async(files, swapped, 0, 0, 0, 0, buf.ctypes.data, n_in,
+                                                           *no_gpu, None, None), "shape")
+    with pytest.raises(atp.AtpError) as e:
+        plan.load_stats()
+    assert e.value.code == atp.ESTATE
     files.close()
     # same shapes, 4-byte elements
     tens, _ = _tensors(c)
