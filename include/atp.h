@@ -111,7 +111,7 @@ typedef struct {
   uint64_t old_offset;
 } atp_tensor;
 
-/* ---- paged KV cache (Sec. III-B: localized by head group per block) ----- */
+/* ---- paged KV cache (Sec. III-B: each token block keeps its heads apart) */
 /* Arena of one rank: [layer][K,V][num_blocks][heads][block_tokens][head_dim]
  * (HEAD_MAJOR) or [layer][K,V][num_blocks][block_tokens][heads][head_dim]
  * (TOKEN_MAJOR), heads = the rank's KV-head range of `space`.  Physical
