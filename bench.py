@@ -359,6 +359,11 @@ def main():
         "assignment": assignment,
         "retained_bytes": int(st.retained_w + st.retained_kv),
         "moved_bytes": int(st.moved_w + st.moved_kv),
+        # in place: hazard levels of the two calls, bytes routed through
+        # staging (cycle breakers and the level chain's tail) and the tail alone
+        "levels": [int(st.n_levels_w), int(st.n_levels_kv)],
+        "staged_bytes": int(st.staged_w + st.staged_kv),
+        "tail_bytes": int(st.tail_w + st.tail_kv),
         "inflow_bytes": int(st.inflow_w + st.inflow_kv),
         "reload_bytes": int(st.global_reload),
         "reload_min_bytes": int(st.reload_min),
