@@ -481,8 +481,9 @@ int atp_load_reshard_weights(atp_plan_t *plan, const atp_st_t *st, const char *c
  * by atp_sync, each once the reads under it have completed, and atp_sync
  * returns once they have landed.  Between the two calls the caller may
  * issue atp_reshard_kv (in place this is the order the library needs, and
- * its KV inflow then uses the link while the weights are read).  `st`,
- * `names` and every buffer must stay valid until atp_sync returns.  Name or
+ * its KV inflow then uses the link while the weights are read).  Every
+ * buffer must stay valid until atp_sync returns; `st` and `names` only
+ * during the call (the reads keep descriptors of their own).  Name or
  * shape errors are ATP_EINVAL before anything starts; a failed read is
  * atp_sync's ATP_EINVAL, after the queued work has drained.  The read
  * statistics come from atp_plan_load_stats after atp_sync. */

@@ -341,6 +341,21 @@ struct LoadJob::Impl {
   std::vector<std::thread> pool;
   std::chrono::steady_clock::time_point t0;
   double read_ms = 0;
+  // duplicates of the files' descriptors, so that the reads never depend
+  // on the caller keeping the opened files (a closed descriptor's number
+  // may already name another file)
+  std::unordered_map<int, int> own_fd;
+  int fd_of(int fd) {
+    auto it = own_fd.find(fd);
+    if (it != own_fd.end()) return it->second;
+    int d = ::dup(fd);
+    if (d < 0) throw Error(ATP_EINVAL, std::string("cannot duplicate a file descriptor: ") + strerror(errno));
+    own_fd[fd] = d;
+    return d;
+  }
+  ~Impl() {
+    for (auto &kv : own_fd) ::close(kv.second);
+  }
 
   void batch_done(size_t b, bool ok) {
     std::lock_guard<std::mutex> g(mu);
@@ -401,7 +416,7 @@ LoadJob::LoadJob(const Plan &P, const StFiles &S, const char *const *names, int 
   for (const atp_segment &s : c.seg_in) {
     const atp_tensor &t = P.tp[size_t(s.tensor)].t;
     const StTensor &f = *ft[size_t(s.tensor)];
-    const int fd = S.fds[size_t(f.file)];
+    const int fd = J.fd_of(S.fds[size_t(f.file)]);
     const uint64_t eb = uint64_t(t.elem_bytes), a = uint64_t(s.unit_begin) * uint64_t(t.unit),
                    b = uint64_t(s.unit_end) * uint64_t(t.unit);
     char *dst = base + s.host_offset;

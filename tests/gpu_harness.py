@@ -60,14 +60,15 @@ def say(msg):
 
 def run_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
              ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False,
-             between=None):
+             between=None, close_files_early=False):
     return prepare_case(c, flags, staging_cap, assign, check_outbound, name, variant, ckpt_dir, evict, pipelined,
-                        sparse_ckpt, kv_first, one_stream, between=between)()()
+                        sparse_ckpt, kv_first, one_stream, between=between,
+                        close_files_early=close_files_early)()()
 
 
 def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=True, name="", variant="cm",
                ckpt_dir=None, evict=None, pipelined=False, sparse_ckpt=False, kv_first=False, one_stream=False,
-               streams=None, between=None):
+               streams=None, between=None, close_files_early=False):
     """Reshard one workload on the GPU and compare with the oracle.  With
     `ckpt_dir`, the weight inflow is read from a safetensors checkpoint
     written there by the library's range-read loader instead of being copied
@@ -193,6 +194,8 @@ def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=Tru
     def weights_call():
         if deferred:
             plan.load_reshard_weights_async(files, ckpt_names, *w_args)
+            if close_files_early:  # the reads keep descriptors of their own
+                files.close()
         elif ckpt_dir is not None and in_w.size and pipelined:
             ls = plan.load_reshard_weights(files, ckpt_names, *w_args)
             assert ls.bytes == in_w.size
@@ -221,7 +224,8 @@ def prepare_case(c, flags=0, staging_cap=0, assign="inorder", check_outbound=Tru
         torch.cuda.synchronize()
         if deferred:
             assert plan.load_stats().bytes == in_w.size
-            files.close()
+            if not close_files_early:
+                files.close()
         got_w = (aw if inplace else nw).cpu().numpy()[:want_w.size]
         got_k = (ak if inplace else nk).cpu().numpy()[:want_k.size]
         bad_w = np.flatnonzero(got_w[mask_w] != want_w[mask_w])

@@ -143,6 +143,17 @@ def test_large_layer_async_from_checkpoint(tmp_path, flags):
 
 
 @pytest.mark.parametrize("flags", [0, atp.INPLACE])
+def test_async_reads_outlive_the_closed_files(tmp_path, flags):
+    """The files are closed right after the asynchronous call, before any read
+    may have run: the reads keep duplicates of the descriptors, so the
+    reshard still gets every byte (a closed descriptor's number could
+    otherwise name another file by then)."""
+    c = configs.scaled(2, layers=1, n_seq=2, seq_tokens=256, w_kind=KIND_TAG16, kv_kind=KIND_TAG16)
+    run_case(c, flags=flags, ckpt_dir=tmp_path, pipelined="async", sparse_ckpt=True, close_files_early=True,
+             name="dense40-1layer-ckpt-async-closed")
+
+
+@pytest.mark.parametrize("flags", [0, atp.INPLACE])
 def test_async_read_failure_is_reported_by_sync(tmp_path, flags):
     """The file is cut short after it was opened: the async call returns, the
     KV call is issued, and atp_sync drains everything queued before it
