@@ -677,8 +677,9 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
       throw Error(ATP_ESTATE, "the device's scratch array is in use by a pending call: atp_sync it first");
     g_scratch_busy[E.device] = true;
   }
-  // from here on the call either is issued (pending) or gives back the
-  // scratch array, once nothing it enqueued can still be running
+  // from here on the call either is issued (pending) or, if it fails after
+  // queuing work, waits until nothing it queued can still be running (the
+  // caller may then free its buffers) and gives back the scratch array
   struct Undo {
     Exec &E;
     CallState &cs;
@@ -686,7 +687,7 @@ void exec_call(Plan &P, bool kvcall, void *arena, uint64_t arena_bytes, void *ne
     bool armed = true, enqueued = false;
     ~Undo() {
       E.no_alloc = false;
-      if (!armed || !cs.on_scratch) return;
+      if (!armed) return;
       if (enqueued)
         for (hipStream_t s : {s0, s1, E.side})
           if (s && hipStreamSynchronize(s) != hipSuccess) (void)hipGetLastError();
