@@ -192,7 +192,9 @@ void atp_plan_free(atp_plan_t *plan);
  * writes the outbound bytes: both host buffers must come from hipHostMalloc
  * (device-accessible at the same address) and be 256-byte aligned, else
  * ATP_EINVAL / ATP_EALIGN.
- * Launch errors return ATP_EHIP; kernel-side errors surface in atp_sync. */
+ * Launch errors return ATP_EHIP once the work the call had already queued
+ * has drained (the plan is then not pending); kernel-side errors surface in
+ * atp_sync. */
 int atp_reshard_weights(atp_plan_t *plan, void *arena, uint64_t arena_bytes,
                         void *new_arena, uint64_t new_arena_bytes,
                         const void *inflow_host, uint64_t inflow_bytes,
